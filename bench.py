@@ -1,0 +1,326 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-layer prefix-reuse prefill step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload l8b_layer]
+                    [--no-pipeline] [--no-cpu-baseline]
+
+Prints ONE JSON line. The timed step is one layer's compute step of the
+Llama-3-8B-shaped batch (4 sequences, 32 q / 8 kv heads, head_dim 128, 4096
+cached + 256 new tokens each) with every input resident in HBM: the plan is
+made once, the cached prefix blocks are loaded once before timing, and each
+step runs append (new K/V into the pool) then paged prefix-prefill attention
+on one stream. `value` = attention FLOPs (causal-exact) / step time.
+
+Reported beside it:
+  roofline      the attention kernel's achieved TFLOP/s (HIP events around each
+                launch) against the bf16 MFMA peak;
+  load          host-to-pool copy of the layer's 64 MiB of cached blocks, per
+                copy method, against a measured contiguous pinned copy;
+  append        the scatter's HBM bytes/s;
+  pipeline      the 32-layer two-stream pipeline: exposed load per layer,
+                the flow-shop least exposure, and their difference;
+  cpu_baseline  the fp64 oracle on a bounded sample of the same layer.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16
+HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
+
+
+def attention_flops(prefix_lens, suffix_lens, num_q_heads, head_dim) -> float:
+    """Causal-exact multiply-add count x2 of QK^T and PV: 4*d per (query, key) pair."""
+    pairs = sum(s * p + s * (s + 1) // 2 for p, s in zip(prefix_lens, suffix_lens))
+    return 4.0 * head_dim * num_q_heads * pairs
+
+
+def load_bytes(prefix_lens, num_kv_heads, head_dim, block_size=16) -> int:
+    """K and V bytes of every cached block (whole blocks move)."""
+    blocks = sum(-(-p // block_size) for p in prefix_lens)
+    return blocks * block_size * num_kv_heads * head_dim * 2 * 2
+
+
+def append_bytes(T, num_kv_heads, head_dim) -> int:
+    """New K and V rows read once and written once."""
+    return 2 * T * num_kv_heads * head_dim * 2 * 2
+
+
+def flow_shop_exposure(load_ms: float, compute_ms: float, n: int) -> float:
+    """Least total exposed load of n layers on two in-order queues (loads back to back,
+    layer l's compute after its load and after layer l-1's compute):
+    makespan = max over l of ((l+1) c + (n-l) p); exposure = makespan - n p."""
+    makespan = max((l + 1) * load_ms + (n - l) * compute_ms for l in range(n))
+    return makespan - n * compute_ms
+
+
+def _median(xs):
+    return float(np.median(np.asarray(xs, dtype=np.float64)))
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _setup_layer(batch, layer=0, method="kernel_pull"):
+    import torch
+    from paper_2603_23049_amd import pcr, synth
+    data = synth.make_layer(batch, layer)
+    Hkv, d, bs = batch.num_kv_heads, batch.head_dim, batch.block_size
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if a.dtype == np.uint16 else a).cuda()
+
+    def pin(a):
+        t = torch.empty(a.shape, dtype=torch.int16, pin_memory=True)
+        t.copy_(torch.from_numpy(a.view(np.int16)))
+        return t
+
+    pool = pcr.KVPool(torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"),
+                      torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"), Hkv, d)
+    host = pcr.HostKV(pin(data.host_k), pin(data.host_v), Hkv, d)
+    src, dst, slots, cu = pcr.plan(batch.prefix_lens, batch.suffix_lens, batch.block_tables, batch.host_blocks, bs)
+    pl = np.asarray(batch.prefix_lens, np.int32)
+    L = pcr.Layer(host, pool, dev(data.q), dev(data.k_new), dev(data.v_new),
+                  torch.zeros(data.q.shape, dtype=torch.int16, device="cuda"))
+    bp = pcr.BatchPlan(src, dst, dev(slots), dev(batch.block_tables), dev(pl), dev(cu), pl, cu,
+                       batch.num_q_heads, 1.0 / math.sqrt(d))
+    return L, bp, data
+
+
+def _attn(L, bp, stream=None):
+    from paper_2603_23049_amd import pcr
+    pcr.prefix_prefill_attn(L.q, L.pool, bp.block_tables, bp.prefix_lens, bp.cu_suffix, bp.host_prefix_lens,
+                            bp.host_cu_suffix, bp.num_q_heads, L.out, sm_scale=bp.sm_scale, stream=stream)
+
+
+def measure_step(batch, steps, warmup):
+    """Timed compute step (append + attention) with prefix KV already in the pool."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    L, bp, _ = _setup_layer(batch)
+    pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="kernel_pull")
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    for _ in range(warmup):
+        pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
+        _attn(L, bp, s)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, m, e in ev:
+        a.record(s)
+        pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
+        m.record(s)
+        _attn(L, bp, s)
+        e.record(s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [a.elapsed_time(e) for a, m, e in ev]
+    append_ms = [a.elapsed_time(m) for a, m, e in ev]
+    attn_ms = [m.elapsed_time(e) for a, m, e in ev]
+    return dict(step_ms=float(np.mean(step_ms)), append_ms=float(np.mean(append_ms)),
+                attn_ms=float(np.mean(attn_ms)), attn_ms_median=_median(attn_ms), wall_s=wall)
+
+
+def measure_load(batch, reps=10):
+    """Host-to-pool copy of one layer's cached blocks, per method; plus a contiguous
+    256 MiB pinned host-to-device copy as the link reference."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    L, bp, _ = _setup_layer(batch)
+    nbytes = load_bytes(batch.prefix_lens, batch.num_kv_heads, batch.head_dim)
+    s = torch.cuda.Stream()
+    out = {"bytes_per_layer": nbytes}
+    for method in ("kernel_pull", "dma_per_block", "dma_batch"):
+        try:
+            times = []
+            for r in range(reps + 2):
+                a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(s)
+                pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method=method, stream=s)
+                e.record(s)
+                e.synchronize()
+                if r >= 2:
+                    times.append(a.elapsed_time(e))
+            ms = _median(times)
+            out[method] = {"ms": ms, "GBps": nbytes / ms / 1e6}
+        except Exception as ex:  # a method this runtime lacks
+            out[method] = {"error": str(ex)[:200]}
+    big = 256 << 20
+    h = torch.empty(big, dtype=torch.uint8, pin_memory=True)
+    h.fill_(1)
+    d = torch.empty(big, dtype=torch.uint8, device="cuda")
+    times = []
+    for r in range(12):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            a.record(s)
+            d.copy_(h, non_blocking=True)
+            e.record(s)
+        e.synchronize()
+        if r >= 2:
+            times.append(a.elapsed_time(e))
+    out["contiguous_h2d_GBps"] = big / _median(times) / 1e6
+    return out
+
+
+def measure_pipeline(batch, method, reps=3):
+    """The n-layer two-stream pipeline; exposure per layer measured and bounded."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    n = batch.num_layers
+    layers = []
+    bp = None
+    for l in range(n):
+        L, bp_l, _ = _setup_layer(batch, l)
+        layers.append(L)
+        bp = bp or bp_l
+    copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
+    runs = []
+    for r in range(reps + 1):
+        t = pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method, timing=True)
+        if r >= 1:
+            runs.append(t)
+    best = min(runs, key=lambda t: t["total_ms"])
+    load_ms = float(np.median(best["load_ms"][1:])) if n > 1 else float(best["load_ms"][0])
+    comp_ms = float(np.median(best["compute_ms"]))
+    e_raw = (best["total_ms"] - best["sum_compute_ms"]) / n
+    e_min = flow_shop_exposure(load_ms, comp_ms, n) / n
+    return {"layers": n, "method": method, "total_ms": best["total_ms"], "sum_compute_ms": best["sum_compute_ms"],
+            "load_ms_per_layer": load_ms, "compute_ms_per_layer": comp_ms,
+            "exposed_ms_per_layer": e_raw, "exposed_min_ms_per_layer": e_min,
+            "exposed_over_min_ms_per_layer": e_raw - e_min,
+            "exposed_over_min_frac_of_load": (e_raw - e_min) / load_ms if load_ms > 0 else None,
+            "exposed_frac_of_load": e_raw / load_ms if load_ms > 0 else None}
+
+
+def cpu_baseline(batch, budget_s=15.0):
+    """The fp64 oracle on a bounded sample of the layer: every head of an evenly spread
+    subset of the suffix tokens, scaled to TFLOP/s by the sample's causal-exact FLOPs."""
+    from oracle import attention as oattn
+    from oracle import datamove as odm
+    from paper_2603_23049_amd import synth
+    data = synth.make_layer(batch, 0)
+    plan = odm.plan(batch.prefix_lens, batch.suffix_lens, batch.block_tables, batch.host_blocks, 16)
+    shape = (batch.pool_blocks, batch.num_kv_heads, 16 * batch.head_dim)
+    pk, pv = odm.pool_after_layer(np.zeros(shape, np.uint16), np.zeros(shape, np.uint16), data.host_k, data.host_v,
+                                  plan, data.k_new, data.v_new)
+    cu = plan[3]
+    Hq, d = batch.num_q_heads, batch.head_dim
+
+    def flops_of(rows):
+        f = 0
+        for t, _ in rows:
+            b = int(np.searchsorted(cu, t, side="right") - 1)
+            f += 4 * d * (batch.prefix_lens[b] + (t - cu[b]) + 1)
+        return float(f)
+
+    stride = 64
+    while True:
+        toks = list(range(0, batch.T, stride))
+        rows = np.array([[t, h] for t in toks for h in range(Hq)], np.int32)
+        t0 = time.perf_counter()
+        oattn.attention(data.q, pk, pv, batch.block_tables, np.asarray(batch.prefix_lens, np.int32), cu,
+                        batch.num_kv_heads, 16, rows=rows)
+        dt = time.perf_counter() - t0
+        if dt * 2 >= budget_s or stride == 1:
+            break
+        stride = max(1, int(stride * dt / budget_s * 1.5) or 1)
+    return {"value": flops_of(rows) / dt / 1e12, "unit": "TFLOP/s", "cores": oattn.num_threads(), "kind": "oracle",
+            "sample": f"every head of every {stride}th suffix token of the layer ({len(rows)} of "
+                      f"{batch.T * Hq} rows), fp64, {dt:.1f} s"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="l8b_layer")
+    ap.add_argument("--no-pipeline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pipeline-method", default="auto")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this path has no cross-GPU exchange and every box here "
+              "has one GPU; run with --gpus 1", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2603_23049_amd import pcr, synth
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    pcr.lib()   # fails loudly if libpcr.so is missing
+
+    batch = synth.REGISTRY[args.workload]()
+    flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
+    _say(f"[bench] step: {args.workload} warmup={args.warmup} steps={args.steps}")
+    st = measure_step(batch, args.steps, args.warmup)
+    value = flops / (st["step_ms"] * 1e-3) / 1e12
+    attn_tflops = flops / (st["attn_ms"] * 1e-3) / 1e12
+    app_b = append_bytes(batch.T, batch.num_kv_heads, batch.head_dim)
+    _say(f"[bench] step {st['step_ms']:.4f} ms, attention {st['attn_ms']:.4f} ms = {attn_tflops:.1f} TFLOP/s")
+
+    _say("[bench] load")
+    load = measure_load(batch)
+    pipe = None
+    if not args.no_pipeline:
+        pbatch = synth.l8b_pipe32()
+        _say(f"[bench] pipeline: {pbatch.name} ({pbatch.num_layers} layers)")
+        pipe = measure_pipeline(pbatch, args.pipeline_method)
+    cpu = None
+    if not args.no_cpu_baseline:
+        _say("[bench] cpu baseline (oracle)")
+        cpu = cpu_baseline(batch)
+
+    rec = {
+        "metric": "prefix-reuse prefill TFLOP/s + % MFMA peak; exposed KV-load ms/layer",
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": st["step_ms"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": batch.B, "num_q_heads": batch.num_q_heads,
+                   "num_kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
+                   "prefix_len": batch.prefix_lens[0], "suffix_len": batch.suffix_lens[0],
+                   "block_size": batch.block_size, "pool_blocks": batch.pool_blocks,
+                   "step": "append + attention, prefix KV resident in HBM"},
+        "mfma_frac": value / MFMA_BF16_PEAK_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": "prefill_attn_kernel", "achieved": attn_tflops,
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
+                     "traffic": None, "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"]},
+        "append": {"ms": st["append_ms"], "bytes": app_b, "GBps": app_b / st["append_ms"] / 1e6,
+                   "frac_hbm": app_b / st["append_ms"] / 1e6 / HBM_PEAK_GBS},
+        "load": load,
+        "pipeline": pipe,
+        "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
+        "cpu_baseline": cpu,
+        "wall_s_timed": st["wall_s"],
+    }
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,240 @@
+/*
+ * pcr.h -- C ABI of libpcr: the per-layer prefix-reuse prefill step on MI355X (gfx950).
+ *
+ * The operation (PCR, Sec. 2.2, 4.3 and 5; Alg. 1): a request's tokens split
+ * into a cached prefix of p tokens, whose K/V already exist in pinned host
+ * memory, and an uncached suffix of s tokens. For every layer, the prefix K/V
+ * blocks are copied into a paged GPU KV pool (Sec. 5: fixed 16-token blocks
+ * mapped through a per-sequence block table, one pool per layer), the
+ * suffix's new K/V rows are written into the pool, and causal attention runs
+ * for the s suffix rows over all p + s keys. With exact prefix matching the
+ * result equals full prefill's output for those rows (Sec. 2.2). A two-stream
+ * pipeline overlaps layer l's compute with the loads of later layers
+ * (Sec. 4.3: only about one layer's load stays exposed when per-layer compute
+ * exceeds per-layer load).
+ *
+ * Conventions for every entry point:
+ *   - Ownership: the caller owns every buffer. Device buffers are plain
+ *     device pointers (e.g. from hipMalloc or a framework allocator); host
+ *     KV stores must be pinned (hipHostMalloc). The library keeps no pointer
+ *     after a call returns.
+ *   - Asynchrony: calls that take a stream only enqueue work on it and do
+ *     not synchronise (pcr_pipeline_run with timing output is the one
+ *     exception). Inputs must stay alive until the stream has passed the work.
+ *   - Streams are hipStream_t values passed as void*; NULL is the default stream.
+ *   - Errors: argument checks run on the host before anything is enqueued and
+ *     return a negative pcr_status; pcr_last_error() then holds a message
+ *     (per thread). Faults inside kernels surface at the caller's next
+ *     synchronisation. No C++ exception crosses this interface.
+ *   - Supported shapes: bf16 K/V/Q, block_size 16, head_dim 64 or 128,
+ *     num_q_heads a multiple of num_kv_heads. Anything else returns
+ *     PCR_ERR_UNSUPPORTED.
+ *   - Empty work (n = 0 pairs, T = 0 tokens, a sequence with s = 0) is a no-op
+ *     returning PCR_OK.
+ *
+ * KV block layout (one layer; K and V are separate arrays of num_blocks blocks;
+ * each block holds num_kv_heads payloads of block_size * head_dim bf16):
+ *   K of (block blk, kv head g, slot o, dim x) at ((blk*Hkv + g)*bs + o)*d + x
+ *   V of (block blk, kv head g, slot o, dim x) at ((blk*Hkv + g)*d + x)*bs + o
+ * Host stores use the same per-block layout, so a load is a bitwise block copy.
+ * Logical token t of sequence b is slot t % bs of pool block block_tables[b][t / bs].
+ * Query head h attends with kv head h / (num_q_heads / num_kv_heads).
+ */
+#ifndef PCR_H_
+#define PCR_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pcr_status {
+    PCR_OK = 0,
+    PCR_ERR_INVALID_ARG = -1,  /* null pointer, bad size, id out of range, inconsistent shapes */
+    PCR_ERR_UNSUPPORTED = -2,  /* valid but unsupported shape (head_dim, block_size, ...) */
+    PCR_ERR_NOT_PINNED = -3,   /* a host KV store is not pinned, device-accessible memory */
+    PCR_ERR_HIP = -4           /* a HIP runtime call failed while enqueuing */
+} pcr_status;
+
+/* One layer's paged KV pool in device memory. */
+typedef struct pcr_kv_pool {
+    void *k;
+    void *v;
+    int32_t num_blocks;
+    int32_t block_size;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+} pcr_kv_pool;
+
+/* One layer's host KV store (pinned host memory, same per-block layout). */
+typedef struct pcr_host_kv {
+    const void *k;
+    const void *v;
+    int64_t num_blocks;
+    int32_t block_size;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+} pcr_host_kv;
+
+/* How pcr_load_kv_layer moves blocks over the host link. */
+typedef enum pcr_load_method {
+    PCR_LOAD_AUTO = 0,          /* the library's default (the measured fastest) */
+    PCR_LOAD_DMA_BATCH = 1,     /* one hipMemcpyBatchAsync per call; runs of consecutive
+                                   blocks merged into one copy */
+    PCR_LOAD_DMA_PER_BLOCK = 2, /* one hipMemcpyAsync per block and per K/V (the
+                                   block-by-block baseline of Sec. 5) */
+    PCR_LOAD_KERNEL_PULL = 3    /* a copy kernel on the given stream reads the pinned host
+                                   pages directly and writes the pool blocks */
+} pcr_load_method;
+
+/*
+ * pcr_plan -- host-side planning of one batch (Alg. 1, planning loop:
+ * each cached block of a scheduled request goes on the host-to-GPU list;
+ * only the unmatched tokens are computed).
+ *
+ * In (host arrays):
+ *   prefix_lens[B], suffix_lens[B]        cached and new token counts (>= 0)
+ *   block_tables[B][max_blocks]           pool block of every logical block; entries
+ *                                         past ceil((p+s)/bs) are ignored
+ *   host_blocks[B][max_host_blocks]       host-store block of every logical prefix
+ *                                         block; entries past ceil(p/bs) are ignored
+ * Out (host arrays, caller-allocated):
+ *   src_blocks[cap_pairs], dst_blocks[cap_pairs], *n_pairs
+ *       the load list, sequence by sequence, logical block ascending; a pair equal
+ *       to an earlier one (a prefix block shared between sequences) is listed once.
+ *       cap_pairs = sum_b ceil(p_b / bs) always suffices.
+ *   slot_mapping[sum_b s_b]   pool slot (block*bs + offset) of each new token,
+ *                             sequences in order
+ *   cu_suffix[B+1]            prefix sums of suffix_lens
+ * Errors (PCR_ERR_INVALID_ARG): a needed block id < 0; a pool block named as the
+ * destination of two different host blocks; a new token's slot already taken, or
+ * inside a pool block another sequence loads; capacity too small.
+ * Touches no GPU.
+ */
+pcr_status pcr_plan(int32_t B, const int32_t *prefix_lens, const int32_t *suffix_lens,
+                    const int32_t *block_tables, int32_t max_blocks,
+                    const int32_t *host_blocks, int32_t max_host_blocks, int32_t block_size,
+                    int32_t *src_blocks, int32_t *dst_blocks, int32_t cap_pairs, int32_t *n_pairs,
+                    int32_t *slot_mapping, int32_t *cu_suffix);
+
+/*
+ * pcr_load_kv_layer -- enqueue the host-to-pool copy of one layer's cached blocks
+ * (Sec. 5: one chunk's blocks land in non-consecutive pool blocks; Alg. 1
+ * "LayerwiseUpload"). For each i < n: pool block dst_blocks[i] of dst (K and V,
+ * all kv heads) becomes a bitwise copy of host block src_blocks[i] of src.
+ * src_blocks / dst_blocks are host arrays, range-checked on the host; dst ids
+ * must be distinct. src must be pinned (PCR_ERR_NOT_PINNED otherwise). Shapes of
+ * src and dst must match. The caller records an event on copy_stream after the
+ * call to order later compute behind the copy.
+ */
+pcr_status pcr_load_kv_layer(const pcr_host_kv *src, const int32_t *src_blocks,
+                             const pcr_kv_pool *dst, const int32_t *dst_blocks, int32_t n,
+                             void *copy_stream);
+
+/* The same, with the copy method chosen by the caller. */
+pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_blocks,
+                                    const pcr_kv_pool *dst, const int32_t *dst_blocks, int32_t n,
+                                    pcr_load_method method, void *copy_stream);
+
+/*
+ * pcr_append_kv -- write the new tokens' K/V into the pool (the KV write that
+ * computing the uncached tokens implies, Sec. 4.3).
+ *   k_new, v_new   device, bf16 [T][Hkv][d] (row-major, contiguous)
+ *   slot_mapping   device, int32 [T]: pool slot of token t (block*bs + offset);
+ *                  slots must be distinct and inside the pool (not re-checked
+ *                  on the device: the values live in device memory)
+ * When a prefix ends inside a block, that block must be loaded before this call
+ * (the load copies the whole block; the append then fills its free slots).
+ */
+pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void *v_new,
+                         const int32_t *slot_mapping, int32_t T, void *stream);
+
+/*
+ * pcr_prefix_prefill_attn -- causal GQA attention of the suffix rows over the
+ * cached prefix plus the suffix, read through the block table (Sec. 2.2, 5).
+ * For sequence b, query head h, suffix row i (absolute position p_b + i), and
+ * keys j in [0, p_b + i]:  out = sum_j softmax_j(sm_scale * <q, k_j>) v_j.
+ *   q              device bf16 [T][Hq][d]; T = cu_suffix[B]
+ *   block_tables   device int32 [B][max_blocks]
+ *   prefix_lens    device int32 [B];  cu_suffix device int32 [B+1]
+ *   host_prefix_lens, host_cu_suffix   host copies of the same (used to size the launch;
+ *                  they must equal the device arrays)
+ *   out            device bf16 [T][Hq][d]; fp32 accumulation, rounded to nearest even
+ * Every key position j <= p_b + s_b - 1 must hold valid data (loaded or appended);
+ * slots past p_b + s_b are never read into the result.
+ */
+pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
+                                   const int32_t *block_tables, int32_t max_blocks,
+                                   const int32_t *prefix_lens, const int32_t *cu_suffix,
+                                   const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
+                                   int32_t B, int32_t num_q_heads, float sm_scale, void *out,
+                                   void *stream);
+
+/*
+ * pcr_gather_kv -- read tokens back out of the pool in logical order (the
+ * staging step of a layer-wise offload, Sec. 4.3; also a test aid).
+ * For each sequence b, tokens starts[b] .. starts[b]+lens[b]-1 go to rows
+ * cu_out[b] .. of k_out / v_out (device bf16 [total][Hkv][d]).
+ *   block_tables device [B][max_blocks]; starts, lens, cu_out device int32
+ *   total = host copy of cu_out[B] (sizes the launch)
+ */
+pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
+                         const int32_t *starts, const int32_t *cu_out, int32_t B, int32_t total,
+                         void *k_out, void *v_out, void *stream);
+
+/* Per-layer device inputs and outputs for pcr_pipeline_run. */
+typedef struct pcr_layer_io {
+    pcr_host_kv host;     /* this layer's pinned host store */
+    pcr_kv_pool pool;     /* this layer's pool */
+    const void *q;        /* device bf16 [T][Hq][d] */
+    const void *k_new;    /* device bf16 [T][Hkv][d] */
+    const void *v_new;    /* device bf16 [T][Hkv][d] */
+    void *out;            /* device bf16 [T][Hq][d] */
+} pcr_layer_io;
+
+/* The batch structure shared by every layer (from pcr_plan). */
+typedef struct pcr_batch {
+    const int32_t *src_blocks;        /* host [n_pairs] */
+    const int32_t *dst_blocks;        /* host [n_pairs] */
+    int32_t n_pairs;
+    const int32_t *slot_mapping;      /* device [T] */
+    int32_t T;
+    const int32_t *block_tables;      /* device [B][max_blocks] */
+    int32_t max_blocks;
+    const int32_t *prefix_lens;       /* device [B] */
+    const int32_t *cu_suffix;         /* device [B+1] */
+    const int32_t *host_prefix_lens;  /* host [B] */
+    const int32_t *host_cu_suffix;    /* host [B+1] */
+    int32_t B;
+    int32_t num_q_heads;
+    float sm_scale;
+} pcr_batch;
+
+/*
+ * pcr_pipeline_run -- the layer-wise overlapped step (Sec. 4.3; Alg. 1
+ * "LayerwiseUpload" and "WaitForUploadEvents"). Every layer's load is enqueued
+ * up front on copy_stream, each followed by an event; compute_stream waits on
+ * layer l's event, then runs layer l's append and attention. Layers are
+ * independent here (each layer's Q and new K/V are inputs).
+ * timing_ms: NULL, or host float[4*n_layers + 2]. When given, the call waits for
+ * the last layer and fills, per layer l: [4l] load ms, [4l+1] compute ms
+ * (append + attention), [4l+2] compute-stream wait before the layer (exposed
+ * load), [4l+3] end of the layer's compute relative to the pipeline start; then
+ * [4n] the whole pipeline ms and [4n+1] the sum of compute ms.
+ */
+pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
+                            pcr_load_method method, void *copy_stream, void *compute_stream,
+                            float *timing_ms);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *pcr_last_error(void);
+
+/* Library version string. */
+const char *pcr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PCR_H_ */

@@ -1,0 +1,232 @@
+// KV data-movement kernels for gfx950: append (new K/V rows into pool slots),
+// gather (pool back to logical order) and the host-pull block copy.
+//
+// All three are pure bit movement; every access is 16 bytes wide where the
+// layout allows, and every block id or slot read from device memory is
+// range-checked in the kernel before use, so a bad table entry skips its row
+// rather than touching memory outside the pool.
+#include "pcr_internal.h"
+
+namespace pcr {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16;
+
+constexpr int kTileTokens = 16;
+
+// ---------------------------------------------------------------------------
+// append: grid (ceil(T/16), Hkv), 256 threads. One workgroup writes 16 new
+// tokens of one kv head. K rows are copied 16 B at a time. V is written
+// d-major inside each block, so the tile is transposed through LDS and each
+// thread then writes 8 consecutive slots of one dim (one 16-B store when the
+// 8 slots are consecutive and 8-aligned, element stores otherwise).
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void append_kv_kernel(
+    u16 *__restrict__ pool_k, u16 *__restrict__ pool_v, int32_t num_blocks, int32_t Hkv,
+    const u16 *__restrict__ k_new, const u16 *__restrict__ v_new,
+    const int32_t *__restrict__ slot_mapping, int32_t T)
+{
+    constexpr int CPR = D / 8;                 // 16-B chunks per row
+    __shared__ u16 vs[kTileTokens][D + 8];     // +8 elements: stagger rows across banks
+    __shared__ int32_t slots[kTileTokens];
+
+    const int tile = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+    const int tok0 = tile * kTileTokens;
+
+    if (tid < kTileTokens) {
+        const int t = tok0 + tid;
+        int32_t sl = -1;
+        if (t < T) {
+            sl = slot_mapping[t];
+            if (sl < 0 || sl / kBlockSize >= num_blocks) sl = -1;
+        }
+        slots[tid] = sl;
+    }
+    __syncthreads();
+
+    if (tid < kTileTokens * CPR) {
+        const int r = tid / CPR, c = tid % CPR;
+        const int t = tok0 + r;
+        if (t < T) {
+            const int64_t src = ((int64_t)t * Hkv + g) * D + c * 8;
+            const u32x4 kv = *reinterpret_cast<const u32x4 *>(k_new + src);
+            const u32x4 vv = *reinterpret_cast<const u32x4 *>(v_new + src);
+            *reinterpret_cast<u32x4 *>(&vs[r][c * 8]) = vv;
+            const int32_t sl = slots[r];
+            if (sl >= 0) {
+                const int64_t blk = sl / kBlockSize, o = sl % kBlockSize;
+                const int64_t dst = ((blk * Hkv + g) * kBlockSize + o) * D + c * 8;
+                *reinterpret_cast<u32x4 *>(pool_k + dst) = kv;
+            }
+        }
+    }
+    __syncthreads();
+
+    // V: thread -> (dim x, half of the tile's tokens)
+    for (int task = tid; task < D * 2; task += 256) {
+        const int x = task / 2, oh = task % 2;
+        const int r0 = oh * 8;
+        const int32_t s0 = slots[r0];
+        bool fast = (s0 >= 0) && (s0 % 8 == 0) && (tok0 + r0 + 7 < T);
+        if (fast) {
+#pragma unroll
+            for (int k = 1; k < 8; ++k) fast = fast && (slots[r0 + k] == s0 + k);
+        }
+        if (fast) {
+            u16 e[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) e[k] = vs[r0 + k][x];
+            u32x4 w;
+            w.x = e[0] | ((unsigned)e[1] << 16);
+            w.y = e[2] | ((unsigned)e[3] << 16);
+            w.z = e[4] | ((unsigned)e[5] << 16);
+            w.w = e[6] | ((unsigned)e[7] << 16);
+            const int64_t blk = s0 / kBlockSize, o = s0 % kBlockSize;
+            *reinterpret_cast<u32x4 *>(pool_v + ((blk * Hkv + g) * D + x) * kBlockSize + o) = w;
+        } else {
+            for (int k = 0; k < 8; ++k) {
+                const int r = r0 + k;
+                const int32_t sl = slots[r];
+                if (tok0 + r < T && sl >= 0) {
+                    const int64_t blk = sl / kBlockSize, o = sl % kBlockSize;
+                    pool_v[((blk * Hkv + g) * D + x) * kBlockSize + o] = vs[r][x];
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// gather: grid (ceil(total/16), Hkv), 256 threads; out rows in logical order.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void gather_kv_kernel(
+    const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v, int32_t num_blocks, int32_t Hkv,
+    const int32_t *__restrict__ block_tables, int32_t max_blocks,
+    const int32_t *__restrict__ starts, const int32_t *__restrict__ cu_out, int32_t B,
+    int32_t total, u16 *__restrict__ k_out, u16 *__restrict__ v_out)
+{
+    constexpr int CPR = D / 8;
+    const int g = blockIdx.y, tid = threadIdx.x;
+    if (tid >= kTileTokens * CPR) return;
+    const int r = blockIdx.x * kTileTokens + tid / CPR, c = tid % CPR;
+    if (r >= total) return;
+    int lo = 0, hi = B - 1;                  // sequence b with cu_out[b] <= r < cu_out[b+1]
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (cu_out[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    const int b = lo;
+    const int t = starts[b] + (r - cu_out[b]);
+    const int64_t dst = ((int64_t)r * Hkv + g) * D + c * 8;
+    u32x4 kw = {0u, 0u, 0u, 0u}, vw = {0u, 0u, 0u, 0u};
+    const int lb = t / kBlockSize;
+    if (t >= 0 && lb < max_blocks) {
+        const int64_t blk = block_tables[(int64_t)b * max_blocks + lb];
+        const int64_t o = t % kBlockSize;
+        if (blk >= 0 && blk < num_blocks) {
+            kw = *reinterpret_cast<const u32x4 *>(pool_k + ((blk * Hkv + g) * kBlockSize + o) * D + c * 8);
+            const u16 *vb = pool_v + ((blk * Hkv + g) * D + c * 8) * kBlockSize + o;
+            u16 e[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) e[k] = vb[k * kBlockSize];
+            vw.x = e[0] | ((unsigned)e[1] << 16);
+            vw.y = e[2] | ((unsigned)e[3] << 16);
+            vw.z = e[4] | ((unsigned)e[5] << 16);
+            vw.w = e[6] | ((unsigned)e[7] << 16);
+        }
+    }
+    *reinterpret_cast<u32x4 *>(k_out + dst) = kw;
+    *reinterpret_cast<u32x4 *>(v_out + dst) = vw;
+}
+
+// ---------------------------------------------------------------------------
+// host pull: each workgroup copies whole blocks (K or V of one pair) from the
+// pinned host store into the pool, 16 B per lane, 8 loads in flight per lane
+// before their stores. Grid-stride over the 2*n block copies.
+// ---------------------------------------------------------------------------
+constexpr int kPullUnroll = 8;
+
+__global__ __launch_bounds__(256) void pull_blocks_kernel(
+    const u32x4 *__restrict__ host_k, const u32x4 *__restrict__ host_v, int64_t host_blocks,
+    u32x4 *__restrict__ pool_k, u32x4 *__restrict__ pool_v, int32_t pool_blocks,
+    int64_t block_vecs, const PullArgs args)
+{
+    const int units = 2 * args.n;
+    for (int u = blockIdx.x; u < units; u += gridDim.x) {
+        const int pair = u >> 1;
+        const bool is_v = u & 1;
+        const int64_t sb = args.src[pair], db = args.dst[pair];
+        if (sb < 0 || sb >= host_blocks || db < 0 || db >= pool_blocks) continue;
+        const u32x4 *src = (is_v ? host_v : host_k) + sb * block_vecs;
+        u32x4 *dst = (is_v ? pool_v : pool_k) + db * block_vecs;
+        for (int64_t base = 0; base < block_vecs; base += 256 * kPullUnroll) {
+            u32x4 r[kPullUnroll];
+#pragma unroll
+            for (int k = 0; k < kPullUnroll; ++k) {
+                const int64_t i = base + k * 256 + threadIdx.x;
+                if (i < block_vecs) r[k] = __builtin_nontemporal_load(src + i);
+            }
+#pragma unroll
+            for (int k = 0; k < kPullUnroll; ++k) {
+                const int64_t i = base + k * 256 + threadIdx.x;
+                if (i < block_vecs) dst[i] = r[k];
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_append_kv(const pcr_kv_pool &pool, const void *k_new, const void *v_new,
+                            const int32_t *slot_mapping, int32_t T, hipStream_t s)
+{
+    const dim3 grid((T + kTileTokens - 1) / kTileTokens, pool.num_kv_heads);
+    auto *pk = static_cast<u16 *>(pool.k);
+    auto *pv = static_cast<u16 *>(pool.v);
+    auto *kn = static_cast<const u16 *>(k_new);
+    auto *vn = static_cast<const u16 *>(v_new);
+    if (pool.head_dim == 128)
+        hipLaunchKernelGGL(append_kv_kernel<128>, grid, dim3(256), 0, s, pk, pv, pool.num_blocks,
+                           pool.num_kv_heads, kn, vn, slot_mapping, T);
+    else
+        hipLaunchKernelGGL(append_kv_kernel<64>, grid, dim3(256), 0, s, pk, pv, pool.num_blocks,
+                           pool.num_kv_heads, kn, vn, slot_mapping, T);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_kv(const pcr_kv_pool &pool, const int32_t *block_tables, int32_t max_blocks,
+                            const int32_t *starts, const int32_t *cu_out, int32_t B, int32_t total,
+                            void *k_out, void *v_out, hipStream_t s)
+{
+    const dim3 grid((total + kTileTokens - 1) / kTileTokens, pool.num_kv_heads);
+    auto *pk = static_cast<const u16 *>(pool.k);
+    auto *pv = static_cast<const u16 *>(pool.v);
+    if (pool.head_dim == 128)
+        hipLaunchKernelGGL(gather_kv_kernel<128>, grid, dim3(256), 0, s, pk, pv, pool.num_blocks,
+                           pool.num_kv_heads, block_tables, max_blocks, starts, cu_out, B, total,
+                           static_cast<u16 *>(k_out), static_cast<u16 *>(v_out));
+    else
+        hipLaunchKernelGGL(gather_kv_kernel<64>, grid, dim3(256), 0, s, pk, pv, pool.num_blocks,
+                           pool.num_kv_heads, block_tables, max_blocks, starts, cu_out, B, total,
+                           static_cast<u16 *>(k_out), static_cast<u16 *>(v_out));
+    return hipGetLastError();
+}
+
+hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t host_blocks,
+                              void *pool_k, void *pool_v, int32_t pool_blocks, int64_t block_bytes,
+                              const PullArgs &args, hipStream_t s)
+{
+    if (args.n <= 0) return hipSuccess;
+    const int units = 2 * args.n;
+    const int grid = units < 64 ? units : 64;
+    hipLaunchKernelGGL(pull_blocks_kernel, dim3(grid), dim3(256), 0, s,
+                       static_cast<const u32x4 *>(host_k), static_cast<const u32x4 *>(host_v),
+                       host_blocks, static_cast<u32x4 *>(pool_k), static_cast<u32x4 *>(pool_v),
+                       pool_blocks, block_bytes / 16, args);
+    return hipGetLastError();
+}
+
+}  // namespace pcr

@@ -1,0 +1,49 @@
+// Internal declarations shared by the libpcr translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/pcr.h"
+
+namespace pcr {
+
+constexpr int kBlockSize = 16;   // tokens per pool block (the serving engine's block, Sec. 5)
+
+// Records a formatted message as this thread's last error and returns `st`.
+pcr_status fail(pcr_status st, const char *fmt, ...);
+// Turns a HIP error into PCR_ERR_HIP with the call site named.
+pcr_status hip_fail(hipError_t e, const char *what);
+
+// Up to this many (src, dst) block pairs travel in one pull-kernel launch as
+// kernel arguments (so no device copy of the host lists is needed).
+constexpr int kPullPairsPerLaunch = 480;
+
+struct PullArgs {
+    int32_t n;
+    int32_t src[kPullPairsPerLaunch];
+    int32_t dst[kPullPairsPerLaunch];
+};
+
+// Kernel launchers (kv_move.hip).
+hipError_t launch_append_kv(const pcr_kv_pool &pool, const void *k_new, const void *v_new,
+                            const int32_t *slot_mapping, int32_t T, hipStream_t s);
+hipError_t launch_gather_kv(const pcr_kv_pool &pool, const int32_t *block_tables, int32_t max_blocks,
+                            const int32_t *starts, const int32_t *cu_out, int32_t B, int32_t total,
+                            void *k_out, void *v_out, hipStream_t s);
+hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t host_blocks,
+                              void *pool_k, void *pool_v, int32_t pool_blocks, int64_t block_bytes,
+                              const PullArgs &args, hipStream_t s);
+
+// Attention launcher (attn.hip).
+hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
+                                      const int32_t *block_tables, int32_t max_blocks,
+                                      const int32_t *prefix_lens, const int32_t *cu_suffix,
+                                      int32_t B, int32_t num_q_heads, int32_t T,
+                                      int32_t max_row_tiles, float sm_scale, void *out,
+                                      hipStream_t s);
+
+// Rows of packed (token, head-in-group) queries one attention workgroup handles.
+int attn_rows_per_workgroup(int head_dim);
+
+}  // namespace pcr

@@ -1,0 +1,286 @@
+"""Thin ctypes binding over libpcr.so with the C ABI's names (include/pcr.h).
+
+Argument marshalling only: tensors become pointers and sizes, streams become
+hipStream_t handles; every step runs inside the library. If libpcr.so is not
+built, or the library reports an error, these functions raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpcr.so")
+
+PCR_OK = 0
+PCR_ERR_INVALID_ARG = -1
+PCR_ERR_UNSUPPORTED = -2
+PCR_ERR_NOT_PINNED = -3
+PCR_ERR_HIP = -4
+
+LOAD_AUTO = 0
+LOAD_DMA_BATCH = 1
+LOAD_DMA_PER_BLOCK = 2
+LOAD_KERNEL_PULL = 3
+LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block": LOAD_DMA_PER_BLOCK,
+                "kernel_pull": LOAD_KERNEL_PULL}
+
+EXPORTS = ["pcr_plan", "pcr_load_kv_layer", "pcr_load_kv_layer_method", "pcr_append_kv",
+           "pcr_prefix_prefill_attn", "pcr_gather_kv", "pcr_pipeline_run", "pcr_last_error",
+           "pcr_version"]
+
+
+class PcrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libpcr status {status}: {message}")
+        self.status = status
+
+
+class _Pool(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_blocks", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32)]
+
+
+class _Host(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_blocks", ctypes.c_int64),
+                ("block_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32)]
+
+
+class _LayerIO(ctypes.Structure):
+    _fields_ = [("host", _Host), ("pool", _Pool), ("q", ctypes.c_void_p), ("k_new", ctypes.c_void_p),
+                ("v_new", ctypes.c_void_p), ("out", ctypes.c_void_p)]
+
+
+class _Batch(ctypes.Structure):
+    _fields_ = [("src_blocks", ctypes.c_void_p), ("dst_blocks", ctypes.c_void_p), ("n_pairs", ctypes.c_int32),
+                ("slot_mapping", ctypes.c_void_p), ("T", ctypes.c_int32), ("block_tables", ctypes.c_void_p),
+                ("max_blocks", ctypes.c_int32), ("prefix_lens", ctypes.c_void_p), ("cu_suffix", ctypes.c_void_p),
+                ("host_prefix_lens", ctypes.c_void_p), ("host_cu_suffix", ctypes.c_void_p),
+                ("B", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("sm_scale", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2603_23049_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.pcr_plan.argtypes = [i32, P, P, P, i32, P, i32, i32, P, P, i32, P, P, P]
+        L.pcr_load_kv_layer.argtypes = [ctypes.POINTER(_Host), P, ctypes.POINTER(_Pool), P, i32, P]
+        L.pcr_load_kv_layer_method.argtypes = [ctypes.POINTER(_Host), P, ctypes.POINTER(_Pool), P, i32,
+                                               ctypes.c_int, P]
+        L.pcr_append_kv.argtypes = [ctypes.POINTER(_Pool), P, P, P, i32, P]
+        L.pcr_prefix_prefill_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, P, P, i32, i32,
+                                              ctypes.c_float, P, P]
+        L.pcr_gather_kv.argtypes = [ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, P, P, P]
+        L.pcr_pipeline_run.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), ctypes.c_int, P, P,
+                                       P]
+        for name in EXPORTS:
+            if name not in ("pcr_last_error", "pcr_version"):
+                getattr(L, name).restype = ctypes.c_int
+        L.pcr_last_error.restype = ctypes.c_char_p
+        L.pcr_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != PCR_OK:
+        raise PcrError(status, lib().pcr_last_error().decode())
+
+
+def last_error() -> str:
+    return lib().pcr_last_error().decode()
+
+
+def version() -> str:
+    return lib().pcr_version().decode()
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _ptr(x) -> Optional[int]:
+    """Address of a torch tensor or numpy array (None stays None)."""
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _i32_host(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+@dataclass
+class KVPool:
+    """One layer's pool: k and v are device tensors of 2-byte elements,
+    shape [num_blocks][num_kv_heads][block_size*head_dim]."""
+    k: "object"
+    v: "object"
+    num_kv_heads: int
+    head_dim: int
+    block_size: int = 16
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self.k.shape[0])
+
+    def c(self) -> _Pool:
+        return _Pool(_ptr(self.k), _ptr(self.v), self.num_blocks, self.block_size, self.num_kv_heads, self.head_dim)
+
+
+@dataclass
+class HostKV:
+    """One layer's pinned host store (same per-block layout as the pool)."""
+    k: "object"
+    v: "object"
+    num_kv_heads: int
+    head_dim: int
+    block_size: int = 16
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self.k.shape[0])
+
+    def c(self) -> _Host:
+        return _Host(_ptr(self.k), _ptr(self.v), self.num_blocks, self.block_size, self.num_kv_heads, self.head_dim)
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def plan(prefix_lens: Sequence[int], suffix_lens: Sequence[int], block_tables, host_blocks, block_size: int = 16):
+    """pcr_plan: returns (src_blocks, dst_blocks, slot_mapping, cu_suffix) as int32 numpy arrays."""
+    pl, sl = _i32_host(prefix_lens), _i32_host(suffix_lens)
+    bt, hb = _i32_host(block_tables), _i32_host(host_blocks)
+    B = int(pl.shape[0])
+    if bt.ndim != 2 or hb.ndim != 2 or bt.shape[0] != B or hb.shape[0] != B:
+        raise ValueError("block_tables and host_blocks must be [B][*]")
+    cap = int(sum(-(-int(p) // block_size) for p in pl))
+    src = np.zeros(max(cap, 1), np.int32)
+    dst = np.zeros(max(cap, 1), np.int32)
+    T = int(sl.sum())
+    slots = np.zeros(max(T, 1), np.int32)
+    cu = np.zeros(B + 1, np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib().pcr_plan(B, _ptr(pl), _ptr(sl), _ptr(bt), bt.shape[1], _ptr(hb), hb.shape[1], block_size,
+                          _ptr(src), _ptr(dst), cap, ctypes.addressof(n), _ptr(slots), _ptr(cu)))
+    return src[:n.value].copy(), dst[:n.value].copy(), slots[:T].copy(), cu
+
+
+def load_kv_layer(src: HostKV, src_blocks, dst: KVPool, dst_blocks, method: str = "auto", stream=None):
+    """pcr_load_kv_layer_method: enqueue the host-to-pool block copies on `stream`."""
+    sb, db = _i32_host(src_blocks), _i32_host(dst_blocks)
+    if sb.shape != db.shape:
+        raise ValueError("src_blocks and dst_blocks differ in length")
+    h, p = src.c(), dst.c()
+    _check(lib().pcr_load_kv_layer_method(ctypes.byref(h), _ptr(sb), ctypes.byref(p), _ptr(db), int(sb.shape[0]),
+                                          LOAD_METHODS[method], _stream(stream)))
+
+
+def append_kv(pool: KVPool, k_new, v_new, slot_mapping, stream=None):
+    """pcr_append_kv: k_new/v_new [T][Hkv][d] and slot_mapping [T] are device tensors."""
+    T = int(k_new.shape[0])
+    p = pool.c()
+    _check(lib().pcr_append_kv(ctypes.byref(p), _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), T, _stream(stream)))
+
+
+def prefix_prefill_attn(q, pool: KVPool, block_tables, prefix_lens, cu_suffix, host_prefix_lens, host_cu_suffix,
+                        num_q_heads: int, out, sm_scale: Optional[float] = None, stream=None):
+    """pcr_prefix_prefill_attn. q/out [T][Hq][d], block_tables [B][max_blocks], prefix_lens [B],
+    cu_suffix [B+1] on the device; host_* are the host copies of the lengths."""
+    hpl, hcu = _i32_host(host_prefix_lens), _i32_host(host_cu_suffix)
+    B = int(hpl.shape[0])
+    if hcu.shape[0] != B + 1:
+        raise ValueError("host_cu_suffix must have B+1 entries")
+    if sm_scale is None:
+        sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    p = pool.c()
+    _check(lib().pcr_prefix_prefill_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
+                                         _ptr(prefix_lens), _ptr(cu_suffix), _ptr(hpl), _ptr(hcu), B,
+                                         int(num_q_heads), float(sm_scale), _ptr(out), _stream(stream)))
+
+
+def gather_kv(pool: KVPool, block_tables, starts, cu_out, total: int, k_out, v_out, stream=None):
+    """pcr_gather_kv: rows of k_out/v_out [total][Hkv][d] from the pool in logical order."""
+    B = int(starts.shape[0])
+    p = pool.c()
+    _check(lib().pcr_gather_kv(ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]), _ptr(starts),
+                               _ptr(cu_out), B, int(total), _ptr(k_out), _ptr(v_out), _stream(stream)))
+
+
+@dataclass
+class Layer:
+    host: HostKV
+    pool: KVPool
+    q: "object"
+    k_new: "object"
+    v_new: "object"
+    out: "object"
+
+
+@dataclass
+class BatchPlan:
+    """Batch structure for the pipeline: host pair lists, device tables and host length copies."""
+    src_blocks: np.ndarray
+    dst_blocks: np.ndarray
+    slot_mapping: "object"       # device int32 [T]
+    block_tables: "object"       # device int32 [B][max_blocks]
+    prefix_lens: "object"        # device int32 [B]
+    cu_suffix: "object"          # device int32 [B+1]
+    host_prefix_lens: np.ndarray
+    host_cu_suffix: np.ndarray
+    num_q_heads: int
+    sm_scale: float
+
+    def c(self) -> _Batch:
+        self._keep = (_i32_host(self.src_blocks), _i32_host(self.dst_blocks), _i32_host(self.host_prefix_lens),
+                      _i32_host(self.host_cu_suffix))
+        sb, db, hpl, hcu = self._keep
+        return _Batch(_ptr(sb), _ptr(db), int(sb.shape[0]), _ptr(self.slot_mapping), int(self.slot_mapping.shape[0]),
+                      _ptr(self.block_tables), int(self.block_tables.shape[1]), _ptr(self.prefix_lens),
+                      _ptr(self.cu_suffix), _ptr(hpl), _ptr(hcu), int(hpl.shape[0]), int(self.num_q_heads),
+                      float(self.sm_scale))
+
+
+def pipeline_run(layers: Sequence[Layer], batch: BatchPlan, copy_stream, compute_stream, method: str = "auto",
+                 timing: bool = False):
+    """pcr_pipeline_run. With timing=True, waits for the last layer and returns a dict of
+    per-layer load/compute/wait ms and totals; otherwise only enqueues and returns None."""
+    n = len(layers)
+    arr = (_LayerIO * max(n, 1))()
+    for i, L in enumerate(layers):
+        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    b = batch.c()
+    t = np.zeros(4 * n + 2, np.float32) if timing else None
+    _check(lib().pcr_pipeline_run(arr, n, ctypes.byref(b), LOAD_METHODS[method], _stream(copy_stream),
+                                  _stream(compute_stream), _ptr(t)))
+    if not timing:
+        return None
+    per = t[:4 * n].reshape(n, 4)
+    return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
+            "end_ms": per[:, 3].copy(), "total_ms": float(t[4 * n]), "sum_compute_ms": float(t[4 * n + 1])}

@@ -1,0 +1,131 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol,
+plans batches exactly as the oracle does, and rejects bad arguments on the
+host before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import datamove as odm
+from paper_2603_23049_amd import pcr, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "pcr.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pcr_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = pcr.lib()
+    declared = _declared_functions()
+    assert "pcr_prefix_prefill_attn" in declared and len(declared) >= 8
+    for name in declared:
+        assert hasattr(L, name), f"{name} declared in pcr.h but not exported"
+    assert set(declared) == set(pcr.EXPORTS)
+    assert "gfx950" in pcr.version()
+
+
+@pytest.mark.parametrize("mk", [synth.tiny, synth.l8b_layer, synth.l70b_pipe80])
+def test_plan_matches_oracle_on_configs(mk):
+    b = mk()
+    want = odm.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, b.block_size)
+    got = pcr.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, b.block_size)
+    for w, g in zip(want, got):
+        assert np.array_equal(w, g)
+
+
+def test_plan_matches_oracle_ragged_shared_and_partial():
+    rng = np.random.Generator(np.random.PCG64(4))
+    for trial in range(50):
+        B = int(rng.integers(1, 6))
+        pl = rng.integers(0, 80, size=B).tolist()
+        sl = rng.integers(0, 40, size=B).tolist()
+        b = synth.ragged_batch("r", Hq=2, Hkv=1, d=64, prefix_lens=pl, suffix_lens=sl, pool_blocks=64,
+                               seed=int(rng.integers(1 << 30)))
+        bt, hb = b.block_tables.copy(), b.host_blocks.copy()
+        if B >= 2 and pl[0] >= 32 and pl[1] >= 32 and trial % 2 == 0:
+            # two sequences share their first two full prefix blocks (same host and pool blocks)
+            bt[1, :2] = bt[0, :2]
+            hb[1, :2] = hb[0, :2]
+        try:
+            want = odm.plan(pl, sl, bt, hb, 16)
+        except odm.PlanError:
+            with pytest.raises(pcr.PcrError) as ei:
+                pcr.plan(pl, sl, bt, hb, 16)
+            assert ei.value.status == pcr.PCR_ERR_INVALID_ARG
+            continue
+        got = pcr.plan(pl, sl, bt, hb, 16)
+        for w, g in zip(want, got):
+            assert np.array_equal(w, g), (trial, pl, sl)
+
+
+def test_plan_rejects_what_the_oracle_rejects():
+    cases = [
+        ([32, 32], [1, 1], [[5, 6, 7], [5, 8, 9]], [[0, 1], [2, 3]]),
+        ([16, 20], [4, 4], [[3, 4], [3, 4]], [[0, -1], [0, 1]]),
+        ([0, 0], [2, 2], [[3], [3]], [[0], [0]]),
+        ([16], [1], [[3, -1]], [[0]]),
+    ]
+    for pl, sl, bt, hb in cases:
+        bt, hb = np.array(bt, np.int32), np.array(hb, np.int32)
+        with pytest.raises(odm.PlanError):
+            odm.plan(pl, sl, bt, hb, 16)
+        with pytest.raises(pcr.PcrError):
+            pcr.plan(pl, sl, bt, hb, 16)
+
+
+def _pool(nb=4, Hkv=1, d=64, bs=16, k=0x10000, v=0x20000):
+    return pcr._Pool(k, v, nb, bs, Hkv, d)
+
+
+def test_argument_validation_before_any_device_work():
+    L = pcr.lib()
+    P = ctypes.byref
+    # unsupported head_dim / block_size
+    assert L.pcr_append_kv(P(_pool(d=96)), 16, 16, 16, 4, None) == pcr.PCR_ERR_UNSUPPORTED
+    assert L.pcr_append_kv(P(_pool(bs=32)), 16, 16, 16, 4, None) == pcr.PCR_ERR_UNSUPPORTED
+    assert "block_size" in pcr.last_error()
+    # null pool pointers, misaligned inputs, negative sizes
+    assert L.pcr_append_kv(P(_pool(k=0)), 16, 16, 16, 4, None) == pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_append_kv(P(_pool()), 18, 16, 16, 4, None) == pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_append_kv(P(_pool()), 16, 16, 16, -1, None) == pcr.PCR_ERR_INVALID_ARG
+    # empty work is a no-op
+    assert L.pcr_append_kv(P(_pool()), None, None, None, 0, None) == pcr.PCR_OK
+    # attention: Hq not a multiple of Hkv, bad scale, too-short block table
+    hpl = np.array([16], np.int32)
+    hcu = np.array([0, 8], np.int32)
+    args = lambda Hq, scale, mb: (16, P(_pool(Hkv=2)), 16, mb, 16, 16, hpl.ctypes.data, hcu.ctypes.data, 1, Hq,
+                                  scale, 16, None)
+    assert L.pcr_prefix_prefill_attn(*args(3, 0.125, 4)) == pcr.PCR_ERR_UNSUPPORTED
+    assert L.pcr_prefix_prefill_attn(*args(4, 0.0, 4)) == pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_prefix_prefill_attn(*args(4, 0.125, 1)) == pcr.PCR_ERR_INVALID_ARG
+    hcu0 = np.array([0, 0], np.int32)
+    assert L.pcr_prefix_prefill_attn(16, P(_pool()), 16, 4, 16, 16, hpl.ctypes.data, hcu0.ctypes.data, 1, 1,
+                                     0.125, 16, None) == pcr.PCR_OK
+    # load: block ids out of range and repeated destinations are caught on the host
+    host = pcr._Host(0x30000, 0x40000, 8, 16, 1, 64)
+    src = np.array([0, 9], np.int32)
+    dst = np.array([1, 2], np.int32)
+    assert L.pcr_load_kv_layer(P(host), src.ctypes.data, P(_pool()), dst.ctypes.data, 2, None) == \
+        pcr.PCR_ERR_INVALID_ARG
+    src = np.array([0, 1], np.int32)
+    dst = np.array([1, 1], np.int32)
+    assert L.pcr_load_kv_layer(P(host), src.ctypes.data, P(_pool()), dst.ctypes.data, 2, None) == \
+        pcr.PCR_ERR_INVALID_ARG
+    assert "twice" in pcr.last_error()
+    assert L.pcr_load_kv_layer(P(host), None, P(_pool()), None, 0, None) == pcr.PCR_OK
+    host_bad = pcr._Host(0x30000, 0x40000, 8, 16, 2, 64)
+    assert L.pcr_load_kv_layer(P(host_bad), src.ctypes.data, P(_pool()), dst.ctypes.data, 2, None) == \
+        pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_load_kv_layer_method(P(host), src.ctypes.data, P(_pool()), dst.ctypes.data, 2, 9, None) == \
+        pcr.PCR_ERR_INVALID_ARG
+    # pipeline: zero layers is a no-op, equal streams are refused
+    assert L.pcr_pipeline_run(None, 0, None, 0, None, None, None) == pcr.PCR_OK
+    lay = (pcr._LayerIO * 1)()
+    bat = pcr._Batch()
+    assert L.pcr_pipeline_run(lay, 1, P(bat), 0, 0x5, 0x5, None) == pcr.PCR_ERR_INVALID_ARG

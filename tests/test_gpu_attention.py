@@ -1,0 +1,134 @@
+"""GPU: prefix-prefill attention through the C ABI against the fp64 oracle.
+
+Tolerance (bf16 inputs, fp32 accumulation, bf16 output): max |err| <= 2e-2 and
+mean |err| <= 2e-3 against the fp64 oracle. Beyond the tolerance the HIP path
+must be deterministic and bit-invariant to which physical blocks hold the KV.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oattn
+from oracle import datamove as odm
+from paper_2603_23049_amd import synth
+from gpuio import GpuLayer, MAX_ABS, MEAN_ABS, error_stats, say, u16
+
+pytestmark = pytest.mark.gpu
+
+BS = 16
+
+
+def _pools(b, seed=99):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    return synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
+
+
+def _oracle(b, data, pk0, pv0, rows=None, block_tables=None, host_blocks=None):
+    bt = b.block_tables if block_tables is None else block_tables
+    hb = b.host_blocks if host_blocks is None else host_blocks
+    plan = odm.plan(b.prefix_lens, b.suffix_lens, bt, hb, BS)
+    pk, pv = odm.pool_after_layer(pk0, pv0, data.host_k, data.host_v, plan, data.k_new, data.v_new, BS)
+    return oattn.attention(data.q, pk, pv, bt, np.asarray(b.prefix_lens, np.int32), plan[3], b.num_kv_heads, BS,
+                           rows=rows)
+
+
+def _run(b, data, pk0, pv0, **kw):
+    L = GpuLayer(b, data, pk0, pv0, **kw)
+    L.run_serial("kernel_pull")
+    return L
+
+
+def _check(got, want, label):
+    mx, mean = error_stats(got, want)
+    say(f"    {label}: max_abs={mx:.3e} mean_abs={mean:.3e}")
+    assert np.all(np.isfinite(got)), label
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{label}: max {mx} mean {mean}"
+
+
+def test_tiny_config_full():
+    b = synth.tiny()
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say("[gpu] attention tiny")
+    L = _run(b, data, pk0, pv0)
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), "tiny")
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("G", [1, 4, 8])
+def test_edge_shapes(d, G):
+    """p in {0,1,15,16,17,256}, s in {1,2,63,64} (all combinations in one ragged batch
+    per (d, G)), plus a long ragged suffix spanning several row tiles."""
+    pl, sl = [], []
+    for p in [0, 1, 15, 16, 17, 256]:
+        for s in [1, 2, 63, 64]:
+            pl.append(p)
+            sl.append(s)
+    pl.append(100)
+    sl.append(300)
+    Hkv = 2
+    nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl)) + 5
+    b = synth.ragged_batch("edges", Hq=Hkv * G, Hkv=Hkv, d=d, prefix_lens=pl, suffix_lens=sl,
+                           pool_blocks=nblocks, seed=10 + d + G)
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention edges d={d} G={G} B={b.B} T={b.T}")
+    L = _run(b, data, pk0, pv0)
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"edges d={d} G={G}")
+
+
+def test_l8b_layer_full_and_deterministic():
+    b = synth.l8b_layer()
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say("[gpu] attention l8b_layer (full oracle)")
+    L = _run(b, data, pk0, pv0)
+    first = u16(L.out).copy()
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), "l8b_layer")
+    L.out.zero_()
+    L.attn()
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(L.out), first), "attention is not deterministic"
+
+
+def test_block_permutation_and_sharing_bit_invariance():
+    """Same logical KV under a different physical block assignment, and with two
+    sequences sharing their common prefix blocks: outputs identical bit for bit."""
+    Hkv, G, d = 2, 4, 128
+    pl, sl = [512, 512, 96], [70, 33, 50]
+    b = synth.ragged_batch("perm", Hq=Hkv * G, Hkv=Hkv, d=d, prefix_lens=pl, suffix_lens=sl, pool_blocks=160,
+                           seed=21)
+    data = synth.make_layer(b)
+    # sequences 0 and 1 hold the same cached prefix (same host blocks)
+    hb = b.host_blocks.copy()
+    hb[1, :32] = hb[0, :32]
+    pk0, pv0 = _pools(b)
+    say("[gpu] attention permutation/sharing")
+    ref = _run(b, data, pk0, pv0, host_blocks=hb)
+    rng = np.random.Generator(np.random.PCG64(5))
+    perm = rng.permutation(b.pool_blocks).astype(np.int32)
+    bt2 = np.where(b.block_tables >= 0, perm[np.maximum(b.block_tables, 0)], -1).astype(np.int32)
+    alt = _run(b, data, pk0, pv0, host_blocks=hb, block_tables=bt2)
+    assert np.array_equal(u16(ref.out), u16(alt.out)), "output depends on physical block ids"
+    bt3 = bt2.copy()
+    bt3[1, :32] = bt3[0, :32]   # shared physical prefix blocks
+    shared = _run(b, data, pk0, pv0, host_blocks=hb, block_tables=bt3)
+    assert len(shared.dst) == len(alt.dst) - 32
+    assert np.array_equal(u16(ref.out), u16(shared.out)), "shared prefix blocks change the output"
+    _check(ref.out_f64(), _oracle(b, data, pk0, pv0, host_blocks=hb), "perm")
+
+
+def test_l70b_shape_sampled_rows():
+    """70B-shaped layer (64 q / 8 kv heads, p=15360, s=1024): every head of a spread of
+    tokens, including the first and last suffix row of both sequences."""
+    b = synth.l70b_pipe80()
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say("[gpu] attention l70b layer 0 (sampled rows)")
+    L = _run(b, data, pk0, pv0)
+    toks = sorted(set([0, 1, 511, 1023, 1024, 1025, 1500, 2047] + list(range(37, 2048, 211))))
+    rows = np.array([[t, h] for t in toks for h in range(b.num_q_heads)], np.int32)
+    want = _oracle(b, data, pk0, pv0, rows=rows)
+    got = L.out_f64()[rows[:, 0], rows[:, 1]]
+    _check(got, want, "l70b sampled")
