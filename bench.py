@@ -252,6 +252,7 @@ def main(argv=None):
     ap.add_argument("--workload", default="l8b_layer")
     ap.add_argument("--no-pipeline", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-load", action="store_true", help="skip the host-to-pool copy measurements")
     ap.add_argument("--pipeline-method", default="auto")
     args = ap.parse_args(argv)
 
@@ -276,8 +277,10 @@ def main(argv=None):
     app_b = append_bytes(batch.T, batch.num_kv_heads, batch.head_dim)
     _say(f"[bench] step {st['step_ms']:.4f} ms, attention {st['attn_ms']:.4f} ms = {attn_tflops:.1f} TFLOP/s")
 
-    _say("[bench] load")
-    load = measure_load(batch)
+    load = None
+    if not args.no_load:
+        _say("[bench] load")
+        load = measure_load(batch)
     pipe = None
     if not args.no_pipeline:
         pbatch = synth.l8b_pipe32()

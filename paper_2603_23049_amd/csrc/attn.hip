@@ -41,6 +41,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -56,6 +57,7 @@ constexpr int kTileKeys = 64;
 constexpr int kTileBlocks = kTileKeys / kBlockSize;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleThreshold = 8.0f;                // log2 units
+constexpr int kXcds = 8;                                 // MI355X: 8 XCDs, workgroups dealt round-robin
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
     const int32_t *__restrict__ prefix_lens, const int32_t *__restrict__ cu_suffix, int32_t Hq,
-    int32_t T, float scale_log2, u16 *__restrict__ out)
+    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, u16 *__restrict__ out)
 {
     using Geo = TileGeom<D>;
     constexpr int CPR = Geo::CPR;
@@ -101,7 +103,16 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // [group][buffer][K tile | V tile]; reused for the merge at the end.
     __shared__ __attribute__((aligned(1024))) char lds[2][2][Geo::BYTES];
 
-    const int rt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    // XCD-aware order: workgroup L runs on XCD L % 8, so consecutive work items
+    // (the row tiles of one (sequence, kv head), which read the same K/V) are
+    // given to workgroups of one XCD and share its L2.
+    const int n_work = row_tiles * Hkv * B;
+    const int per_xcd = (int)(gridDim.x / kXcds);
+    const int w = (int)(blockIdx.x % kXcds) * per_xcd + (int)(blockIdx.x / kXcds);
+    if (w >= n_work) return;
+    const int rt = w % row_tiles;
+    const int g = (w / row_tiles) % Hkv;
+    const int b = w / (row_tiles * Hkv);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2;              // 0: first half of the keys, 1: second half
@@ -161,8 +172,24 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 
     const int32_t *bt = block_tables + (int64_t)b * max_blocks;
 
-    // Issue the direct loads of tile kt into (this group's) buffer buf.
-    auto issue_tile = [&](int kt, int buf) {
+    // Block ids of one tile (4 pool blocks), read as scalars; ids past the
+    // sequence or outside the pool become block 0 (their keys are masked and
+    // their V entries zeroed), so no load ever leaves the pool.
+    auto tile_ids = [&](int kt, int32_t (&ids)[kTileBlocks]) {
+#pragma unroll
+        for (int j = 0; j < kTileBlocks; ++j) {
+            const int lb = kt * kTileBlocks + j;
+            int32_t blk = 0;
+            if (lb < valid_blocks) {
+                blk = bt[lb];
+                if (blk < 0 || blk >= num_blocks) blk = 0;
+            }
+            ids[j] = blk;
+        }
+    };
+
+    // Issue the direct loads of a tile (block ids given) into this group's buffer buf.
+    auto issue_tile = [&](const int32_t (&ids)[kTileBlocks], int buf) {
         char *tbase = lds[grp][buf];
 #pragma unroll
         for (int u = 0; u < Geo::LOADS; ++u) {
@@ -171,13 +198,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             const int P = slab * 64 + lane;                        // 16-B chunk position in the tile
             const int Pk = is_k ? P : P - Geo::KBYTES / 16;
             const int j = is_k ? (slab * 64) / (CPR * kBlockSize) : ((slab - Geo::KSLABS) * 64) / (2 * D);
-            const int lb = kt * kTileBlocks + j;
-            int32_t blk = 0;
-            if (lb < valid_blocks) {
-                blk = bt[lb];
-                if (blk < 0 || blk >= num_blocks) blk = 0;         // never read outside the pool
-            }
-            const int64_t head_base = ((int64_t)blk * Hkv + g) * kHeadPayload;
+            const int64_t head_base = ((int64_t)ids[j] * Hkv + g) * kHeadPayload;
             const u16 *src;
             if (is_k) {
                 const int key = Pk / CPR, pc = Pk % CPR;
@@ -211,27 +232,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         }
     };
 
-    const int last_tile = ntiles - 1;
-    const bool last_needs_zero = (last_tile + 1) * kTileKeys > total;
-    const int last_owner = last_tile >= split ? 1 : 0;
-    const int last_iter = last_tile - (last_owner ? split : 0);
-
-    if (tile_begin < tile_end) issue_tile(tile_begin, 0);
-
-    for (int it = 0; it < niter; ++it) {
-        const int buf = it & 1;
-        const int kt = tile_begin + it;
-        const bool have = kt < tile_end;
-        wait_vmem();
-        __syncthreads();
-        if (last_needs_zero && it == last_iter) {                  // uniform over the workgroup
-            if (grp == last_owner) zero_tail(kt, buf);
-            __syncthreads();
-        }
-        if (have && kt + 1 < tile_end) issue_tile(kt + 1, buf ^ 1);
+    // One tile's math for this wave. masked: some key of the tile lies past some
+    // row's causal limit (only the last tiles of a row range; wave-uniform).
+    auto compute_tile = [&](bool masked, int kt, int buf) {
         const int kbase = kt * kTileKeys;
-        if (!have || kbase > w_max_limit) continue;
-
         const char *tk = lds[grp][buf];
         const char *tv = tk + Geo::KBYTES;
         // ---- S^T = K Q^T over two 32-key halves ----
@@ -249,23 +253,20 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             }
         }
         // ---- online softmax (log2 domain, lazy rescale) ----
-        const bool need_mask = kbase + kTileKeys - 1 > w_min_limit;
-        float mx = -INFINITY;
-        if (need_mask) {
+        if (masked) {
+            // register r of half tile m holds key kbase + 32m + 16(r/8) + 8half + r%8
+            const int lim = limit - kbase - 8 * half;
 #pragma unroll
             for (int m = 0; m < 2; ++m)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = kbase + 32 * m + 16 * (r >> 3) + 8 * half + (r & 7);
-                    if (key > limit) st[m][r] = -INFINITY;
-                    mx = fmaxf(mx, st[m][r]);
-                }
-        } else {
-#pragma unroll
-            for (int m = 0; m < 2; ++m)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[m][r]);
+                for (int r = 0; r < 16; ++r)
+                    st[m][r] = (32 * m + 16 * (r >> 3) + (r & 7)) > lim ? -INFINITY : st[m][r];
         }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(st[m][r], st[m][r + 1]));
         mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
         if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold)) {
             const float m_new = fmaxf(m_run, mx);
@@ -277,25 +278,23 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) o_acc[mt][r] *= alpha;
         }
+        // A row with no key yet has m_run = -inf and only masked scores: exp2(-inf) = 0.
         const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-        float psum = 0.f;
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(st[m][r], scale_log2, neg_m));
-                if (need_mask) pe = (st[m][r] == -INFINITY) ? 0.f : pe;
-                st[m][r] = pe;
-                psum += pe;
-            }
-        l_run += psum;
-        // ---- O^T += V^T P^T, k-step t = pool block t of the tile ----
+        // ---- per pool block t of the tile: P = exp2(s*scale - m) in bf16, row sums from
+        // the bf16 values the MFMA uses, then O^T += V^T P^T (k-step t) ----
+        const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
         for (int t = 0; t < kTileBlocks; ++t) {
             f32x8 pv;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pv[e] = st[t >> 1][8 * (t & 1) + e];
+            for (int e = 0; e < 8; ++e)
+                pv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[t >> 1][8 * (t & 1) + e], scale_log2, neg_m));
             const bf16x8 pf = __builtin_convertvector(pv, bf16x8);
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const bf16x2_t pair = {pf[e], pf[e + 1]};
+                l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+            }
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 const int d = 32 * mt + qc;
@@ -305,6 +304,36 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, o_acc[mt], 0, 0, 0);
             }
         }
+    };
+
+    const int last_tile = ntiles - 1;
+    const bool last_needs_zero = (last_tile + 1) * kTileKeys > total;
+    const int last_owner = last_tile >= split ? 1 : 0;
+    const int last_iter = last_tile - (last_owner ? split : 0);
+
+    int32_t ids[kTileBlocks];
+    if (tile_begin < tile_end) {
+        tile_ids(tile_begin, ids);
+        issue_tile(ids, 0);
+        if (tile_begin + 1 < tile_end) tile_ids(tile_begin + 1, ids);
+    }
+
+    for (int it = 0; it < niter; ++it) {
+        const int buf = it & 1;
+        const int kt = tile_begin + it;
+        const bool have = kt < tile_end;
+        wait_vmem();
+        __syncthreads();
+        if (last_needs_zero && it == last_iter) {                  // uniform over the workgroup
+            if (grp == last_owner) zero_tail(kt, buf);
+            __syncthreads();
+        }
+        if (have && kt + 1 < tile_end) {
+            issue_tile(ids, buf ^ 1);                              // ids of tile kt+1
+            if (kt + 2 < tile_end) tile_ids(kt + 2, ids);
+        }
+        if (!have || kt * kTileKeys > w_max_limit) continue;
+        compute_tile(kt * kTileKeys + kTileKeys - 1 > w_min_limit, kt, buf);
     }
 
     // ---- merge the two key halves through LDS, normalise, store ----
@@ -364,7 +393,8 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s)
 {
-    const dim3 grid(max_row_tiles, pool.num_kv_heads, B);
+    const int64_t n_work = (int64_t)max_row_tiles * pool.num_kv_heads * B;
+    const dim3 grid((unsigned)(((n_work + kXcds - 1) / kXcds) * kXcds));
     const float scale_log2 = sm_scale * kLog2e;
     auto *qq = static_cast<const u16 *>(q);
     auto *pk = static_cast<const u16 *>(pool.k);
@@ -373,11 +403,11 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
     if (pool.head_dim == 128)
         hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, scale_log2, oo);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo);
     else
         hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, scale_log2, oo);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo);
     return hipGetLastError();
 }
 
