@@ -34,6 +34,8 @@
 // XOR-swizzled so that lanes reading 32 different key rows (K) or dims (V)
 // hit distinct banks; the swizzle is applied through the source address of
 // each lane, since a direct load writes lane l's 16 bytes at base + 16*l.
+#include <type_traits>
+
 #include "pcr_internal.h"
 
 namespace pcr {
@@ -79,13 +81,32 @@ struct TileGeom {
     static constexpr int CPR = D / 8;                          // 16-B chunks per K row
     static constexpr int KBYTES = kTileKeys * D * 2;           // K tile bytes
     static constexpr int VBYTES = kTileKeys * D * 2;           // V tile bytes
-    static constexpr int BYTES = KBYTES + VBYTES;
-    static constexpr int SLABS = BYTES / 1024;                 // 1 KB per wave-wide direct load
-    static constexpr int LOADS = SLABS / kGroupWaves;          // direct loads per thread per tile
-    static constexpr int KSLABS = KBYTES / 1024;
+    static constexpr int KLOADS = KBYTES / 1024 / kGroupWaves; // 1 KB direct loads per thread, K tile
+    static constexpr int VLOADS = VBYTES / 1024 / kGroupWaves; // same, V tile
 };
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier without a memory fence. The phase schedule orders its memory
+// traffic explicitly: every direct load is waited for (vmcnt) by the wave that
+// issued it before the barrier that precedes its first reader, and every LDS read
+// is consumed before its wave reaches the next barrier. The empty asm statements
+// keep the compiler from moving memory operations across the barrier.
+__device__ __forceinline__ void phase_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (the N most recent may still be in flight).
+template <int N>
+__device__ __forceinline__ void wait_vmem_keep()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
@@ -99,9 +120,11 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     constexpr int KSTEPS = D / 16;
     constexpr int MT = D / 32;
     constexpr int64_t kHeadPayload = kBlockSize * D;
+    constexpr int kKLoads = Geo::KLOADS, kVLoads = Geo::VLOADS;
 
-    // [group][buffer][K tile | V tile]; reused for the merge at the end.
-    __shared__ __attribute__((aligned(1024))) char lds[2][2][Geo::BYTES];
+    // Per group: K buffers 0/1 then V buffers 0/1 (double-buffered, tile j in buffer j&1);
+    // the whole array is reused for the merge at the end.
+    __shared__ __attribute__((aligned(1024))) char lds[2][2 * (Geo::KBYTES + Geo::VBYTES)];
 
     // XCD-aware order: workgroup L runs on XCD L % 8, so consecutive work items
     // (the row tiles of one (sequence, kv head), which read the same K/V) are
@@ -140,16 +163,16 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int wg_last = min(rows_total - 1, row0 + kRowsPerWG - 1);
     const int ntiles = (p + wg_last / G) / kTileKeys + 1;
     const int split = (ntiles + 1) >> 1;             // group 0: [0, split), group 1: [split, ntiles)
-    const int niter = split;
     const int tile_begin = grp ? split : 0;
-    const int tile_end = grp ? ntiles : split;
+    const int n = (grp ? ntiles : split) - tile_begin;   // this group's tiles
     const int w_first = min(rows_total - 1, row0 + wg * kRowsPerWave);
     const int w_last = min(rows_total - 1, row0 + wg * kRowsPerWave + kRowsPerWave - 1);
     const int w_min_limit = p + w_first / G;
-    const int w_max_limit = p + w_last / G;
     const int valid_blocks = min((total + kBlockSize - 1) / kBlockSize, max_blocks);
 
-    // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row).
+    // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row),
+    // pre-multiplied by sm_scale*log2(e) so that the first product yields log2-domain
+    // scores directly.
     bf16x8 qf[KSTEPS];
     {
         const bool ok = tq < T;
@@ -158,7 +181,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         for (int ks = 0; ks < KSTEPS; ++ks) {
             u32x4 v = {0u, 0u, 0u, 0u};
             if (ok) v = *reinterpret_cast<const u32x4 *>(qrow + 16 * ks + 8 * half);
-            qf[ks] = as_bf16x8(v);
+            f32x8 f = __builtin_convertvector(as_bf16x8(v), f32x8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) f[e] *= scale_log2;
+            qf[ks] = __builtin_convertvector(f, bf16x8);
         }
     }
 
@@ -167,93 +193,175 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o_acc[mt][r] = 0.f;
-    float m_run = -INFINITY;   // reference max of raw scores times scale_log2
+    // Scores are kept relative to a reference m_ref (log2 domain): the first product
+    // starts from -m_ref, so S^T holds scale*log2(e)*<q,k> - m_ref and P = exp2(S^T).
+    float m_ref = 0.f;
+    bool has_ref = false;      // m_ref has been set from a real score
     float l_run = 0.f;         // this lane's part of the denominator
+    f32x16 nbias;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) nbias[r] = 0.f;
 
     const int32_t *bt = block_tables + (int64_t)b * max_blocks;
+    auto kbuf = [&](int j) { return &lds[grp][(j & 1) * Geo::KBYTES]; };
+    auto vbuf = [&](int j) { return &lds[grp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
 
-    // Block ids of one tile (4 pool blocks), read as scalars; ids past the
-    // sequence or outside the pool become block 0 (their keys are masked and
-    // their V entries zeroed), so no load ever leaves the pool.
-    auto tile_ids = [&](int kt, int32_t (&ids)[kTileBlocks]) {
+    // Pool block ids of this group's tile j, read raw (as scalars) one phase before
+    // use; logical blocks past the sequence read nothing. The range check happens at
+    // use, so the scalar loads are never waited for on the spot: an id past the
+    // sequence or outside the pool becomes block 0 (its keys are masked and its V
+    // entries cleared before use), so no load ever leaves the pool.
+    auto tile_ids = [&](int j, int32_t (&ids)[kTileBlocks]) {
 #pragma unroll
-        for (int j = 0; j < kTileBlocks; ++j) {
-            const int lb = kt * kTileBlocks + j;
-            int32_t blk = 0;
-            if (lb < valid_blocks) {
-                blk = bt[lb];
-                if (blk < 0 || blk >= num_blocks) blk = 0;
-            }
-            ids[j] = blk;
+        for (int jb = 0; jb < kTileBlocks; ++jb) {
+            const int lb = (tile_begin + j) * kTileBlocks + jb;
+            ids[jb] = lb < valid_blocks ? bt[lb] : 0;
         }
     };
+    auto checked = [&](int32_t blk) { return (blk < 0 || blk >= num_blocks) ? 0 : blk; };
 
-    // Issue the direct loads of a tile (block ids given) into this group's buffer buf.
-    auto issue_tile = [&](const int32_t (&ids)[kTileBlocks], int buf) {
-        char *tbase = lds[grp][buf];
+    // Direct loads of this group's tile j (K or V) into its buffer; 1 KB slab per
+    // wave-wide load; the LDS swizzle is applied through each lane's source.
+    // One direct load (load u of the tile's K or V) of this group's tile j into its buffer:
+    // a 1 KB slab per wave-wide load; the LDS swizzle is applied through each lane's source.
+    auto load_k = [&](int j, const int32_t (&ids)[kTileBlocks], int u) {
+        const int slab = u * kGroupWaves + wg;                             // wave-uniform
+        const int jb = (slab * 64) / (CPR * kBlockSize);                   // pool block of the slab
+        const int P = slab * 64 + lane;
+        const int key = P / CPR, pc = P % CPR;
+        const int c = pc ^ k_swizzle<CPR>(key);
+        const int64_t head_base = ((int64_t)checked(ids[jb]) * Hkv + g) * kHeadPayload;
+        const u16 *src = pool_k + head_base + (key % kBlockSize) * D + c * 8;
+        __builtin_amdgcn_global_load_lds(
+            (const void *)src, (__attribute__((address_space(3))) void *)(kbuf(j) + slab * 1024), 16, 0, 0);
+    };
+    auto load_v = [&](int j, const int32_t (&ids)[kTileBlocks], int u) {
+        const int slab = u * kGroupWaves + wg;
+        const int jb = (slab * 64) / (2 * D);
+        const int within = (slab * 64 + lane) % (2 * D);
+        const int d = within >> 1, pch = within & 1;
+        const int ch = pch ^ ((d >> 3) & 1);
+        const int64_t head_base = ((int64_t)checked(ids[jb]) * Hkv + g) * kHeadPayload;
+        const u16 *src = pool_v + head_base + d * kBlockSize + ch * 8;
+        __builtin_amdgcn_global_load_lds(
+            (const void *)src, (__attribute__((address_space(3))) void *)(vbuf(j) + slab * 1024), 16, 0, 0);
+    };
+    auto issue_k = [&](int j, const int32_t (&ids)[kTileBlocks]) {
 #pragma unroll
-        for (int u = 0; u < Geo::LOADS; ++u) {
-            const int slab = u * kGroupWaves + wg;                 // wave-uniform
-            const bool is_k = slab < Geo::KSLABS;                  // wave-uniform
-            const int P = slab * 64 + lane;                        // 16-B chunk position in the tile
-            const int Pk = is_k ? P : P - Geo::KBYTES / 16;
-            const int j = is_k ? (slab * 64) / (CPR * kBlockSize) : ((slab - Geo::KSLABS) * 64) / (2 * D);
-            const int64_t head_base = ((int64_t)ids[j] * Hkv + g) * kHeadPayload;
-            const u16 *src;
-            if (is_k) {
-                const int key = Pk / CPR, pc = Pk % CPR;
-                const int c = pc ^ k_swizzle<CPR>(key);
-                src = pool_k + head_base + (key % kBlockSize) * D + c * 8;
-            } else {
-                const int within = Pk % (2 * D);
-                const int d = within >> 1, pch = within & 1;
-                const int ch = pch ^ ((d >> 3) & 1);
-                src = pool_v + head_base + d * kBlockSize + ch * 8;
-            }
-            __builtin_amdgcn_global_load_lds(
-                (const void *)src, (__attribute__((address_space(3))) void *)(tbase + slab * 1024), 16, 0, 0);
-        }
+        for (int u = 0; u < kKLoads; ++u) load_k(j, ids, u);
+    };
+    auto issue_v = [&](int j, const int32_t (&ids)[kTileBlocks]) {
+#pragma unroll
+        for (int u = 0; u < kVLoads; ++u) load_v(j, ids, u);
     };
 
-    // Zero the V entries of keys >= total in a tile's buffer (their slots may hold
-    // anything, and a zero probability times a NaN would still poison the sum).
-    auto zero_tail = [&](int kt, int buf) {
-        u16 *vt = reinterpret_cast<u16 *>(lds[grp][buf] + Geo::KBYTES);
-        const int gtid = tid & 255;
-        for (int e = gtid; e < kTileBlocks * D; e += 256) {       // one (block, dim) row of 16 keys
-            const int j = e / D, d = e % D;
-            const int key0 = kt * kTileKeys + j * kBlockSize;
-#pragma unroll
-            for (int o = 0; o < kBlockSize; ++o)
-                if (key0 + o >= total) {
-                    const int pch = (o >> 3) ^ ((d >> 3) & 1);
-                    vt[(j * D + d) * kBlockSize + pch * 8 + (o & 7)] = 0;
-                }
-        }
-    };
-
-    // One tile's math for this wave. masked: some key of the tile lies past some
-    // row's causal limit (only the last tiles of a row range; wave-uniform).
-    auto compute_tile = [&](bool masked, int kt, int buf) {
-        const int kbase = kt * kTileKeys;
-        const char *tk = lds[grp][buf];
-        const char *tv = tk + Geo::KBYTES;
-        // ---- S^T = K Q^T over two 32-key halves ----
-        f32x16 st[2];
+    // ---- matrix work: S^T(j) = K(j) Q^T over two 32-key halves ----
+    auto qk = [&](int j, f32x16 (&st)[2]) {
+        const char *tk = kbuf(j);
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) st[m][r] = 0.f;
             const int krow = 32 * m + key_of_row(qc);
 #pragma unroll
             for (int ks = 0; ks < KSTEPS; ++ks) {
                 const int pc = (2 * ks + half) ^ k_swizzle<CPR>(krow);
                 const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(tk + (krow * CPR + pc) * 16));
-                st[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], st[m], 0, 0, 0);
+                st[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], ks == 0 ? nbias : st[m], 0, 0, 0);
             }
         }
-        // ---- online softmax (log2 domain, lazy rescale) ----
-        if (masked) {
+    };
+
+    // ---- matrix work: O^T += V^T(j) P^T(j), k-step t = pool block t of the tile.
+    // In the tile holding the sequence end, V entries of keys >= total are cleared
+    // in the operand (their slots may hold anything; 0 * NaN would poison O).
+    auto pv = [&](int j, const bf16x8 (&pf)[kTileBlocks], auto clear_tag) {
+        constexpr bool CLEAR = decltype(clear_tag)::value;
+        const char *tv = vbuf(j);
+        const int vlim = total - (tile_begin + j) * kTileKeys;     // valid keys in the tile
+#pragma unroll
+        for (int t = 0; t < kTileBlocks; ++t) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const int d = 32 * mt + qc;
+                const int pch = half ^ ((d >> 3) & 1);
+                u32x4 raw = *reinterpret_cast<const u32x4 *>(tv + ((t * D + d) * 2 + pch) * 16);
+                if constexpr (CLEAR) {
+                    const int nvalid = vlim - 16 * t - 8 * half;   // valid keys among this lane's 8
+#pragma unroll
+                    for (int wd = 0; wd < 4; ++wd)
+                        raw[wd] &= (2 * wd < nvalid ? 0x0000FFFFu : 0u) | (2 * wd + 1 < nvalid ? 0xFFFF0000u : 0u);
+                }
+                o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(raw), pf[t], o_acc[mt], 0, 0, 0);
+            }
+        }
+    };
+
+    // ---- matrix cluster: PV(j) (optional) then QK(j+1) (optional) as one stream of
+    // (LDS fragment, MFMA) pairs, the fragment reads running kAhead pairs ahead (a single
+    // wave gets about one 1 KB LDS read per MFMA time, so reads must stay in flight
+    // behind the MFMAs). When QK runs, the cluster also issues the direct loads of
+    // V(j+1) and K(j+2), one per few MFMAs, so the texture path never backs up a wave.
+    auto matrix_cluster = [&](auto pv_tag, auto qk_tag, int j, const bf16x8 (&pf)[kTileBlocks],
+                              f32x16 (&st)[2], const int32_t (&idv)[kTileBlocks],
+                              const int32_t (&idk)[kTileBlocks]) {
+        constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
+        constexpr int NPV = DO_PV ? kTileBlocks * MT : 0, NQK = DO_QK ? 2 * KSTEPS : 0, NALL = NPV + NQK;
+        constexpr int NLD = DO_QK ? kVLoads + kKLoads : 0;
+        constexpr int EVERY = NLD ? (NALL / NLD > 0 ? NALL / NLD : 1) : 1;
+        constexpr int kAhead = 4;
+        const char *tv = vbuf(j);
+        const char *tk = kbuf(j + 1);
+        auto frag = [&](int i) -> u32x4 {
+            if (i < NPV) {
+                const int t = i / MT, mt = i % MT;
+                const int d = 32 * mt + qc;
+                const int pch = half ^ ((d >> 3) & 1);
+                return *reinterpret_cast<const u32x4 *>(tv + ((t * D + d) * 2 + pch) * 16);
+            }
+            const int m = (i - NPV) / KSTEPS, ks = (i - NPV) % KSTEPS;
+            const int krow = 32 * m + key_of_row(qc);
+            const int pc = (2 * ks + half) ^ k_swizzle<CPR>(krow);
+            return *reinterpret_cast<const u32x4 *>(tk + (krow * CPR + pc) * 16);
+        };
+        u32x4 fr[NALL];
+#pragma unroll
+        for (int i = 0; i < kAhead && i < NALL; ++i) fr[i] = frag(i);
+        int ld = 0;
+#pragma unroll
+        for (int i = 0; i < NALL; ++i) {
+            if (i + kAhead < NALL) fr[i + kAhead] = frag(i + kAhead);
+            if (i < NPV) {
+                const int t = i / MT, mt = i % MT;
+                o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i]), pf[t], o_acc[mt], 0, 0, 0);
+            } else {
+                const int m = (i - NPV) / KSTEPS, ks = (i - NPV) % KSTEPS;
+                st[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i]), qf[ks], ks == 0 ? nbias : st[m],
+                                                                0, 0, 0);
+            }
+            if (NLD && i % EVERY == EVERY - 1 && ld < NLD) {
+                if (ld < kVLoads) load_v(j + 1, idv, ld);
+                else load_k(j + 2, idk, ld - kVLoads);
+                ++ld;
+            }
+        }
+        // keep that schedule: the first reads, then (read, MFMA[, load]) groups, then the last MFMAs
+#pragma unroll
+        for (int i = 0; i < kAhead && i < NALL; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        int ld2 = 0;
+#pragma unroll
+        for (int i = 0; i < NALL; ++i) {
+            if (i + kAhead < NALL) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (NLD && i % EVERY == EVERY - 1 && ld2 < NLD) {
+                __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+                ++ld2;
+            }
+        }
+    };
+
+    // ---- vector work: online softmax of S^T(j) into bf16 P(j) (log2 domain, lazy rescale) ----
+    auto softmax = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+        const int kbase = (tile_begin + j) * kTileKeys;
+        if (kbase + kTileKeys - 1 > w_min_limit) {
             // register r of half tile m holds key kbase + 32m + 16(r/8) + 8half + r%8
             const int lim = limit - kbase - 8 * half;
 #pragma unroll
@@ -267,79 +375,111 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         for (int m = 0; m < 2; ++m)
 #pragma unroll
             for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(st[m][r], st[m][r + 1]));
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
-        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold)) {
-            const float m_new = fmaxf(m_run, mx);
-            const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
+        {   // the other half-wave holds the other 32 keys of the same query
+            const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
+                                                             __builtin_bit_cast(unsigned, mx), false, false);
+            mx = fmaxf(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+        }
+        // Move the reference up when the tile's max exceeds it by more than 2^8, or set it
+        // from the first real score; keeps P <= 256 without rescaling O on most tiles.
+        const bool need = (mx > kRescaleThreshold) || (!has_ref && mx > -INFINITY);
+        if (__builtin_amdgcn_ballot_w64(need)) {
+            const float delta = need ? mx : 0.f;
+            const float alpha = __builtin_amdgcn_exp2f(-delta);
+            has_ref = has_ref || need;
+            m_ref += delta;
             l_run *= alpha;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) o_acc[mt][r] *= alpha;
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) st[m][r] -= delta;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) nbias[r] = -m_ref;
         }
-        // A row with no key yet has m_run = -inf and only masked scores: exp2(-inf) = 0.
-        const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-        // ---- per pool block t of the tile: P = exp2(s*scale - m) in bf16, row sums from
-        // the bf16 values the MFMA uses, then O^T += V^T P^T (k-step t) ----
         const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
         for (int t = 0; t < kTileBlocks; ++t) {
-            f32x8 pv;
+            f32x8 pv8;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                pv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[t >> 1][8 * (t & 1) + e], scale_log2, neg_m));
-            const bf16x8 pf = __builtin_convertvector(pv, bf16x8);
+                pv8[e] = __builtin_amdgcn_exp2f(st[t >> 1][8 * (t & 1) + e]);
+            pf[t] = __builtin_convertvector(pv8, bf16x8);
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const bf16x2_t pair = {pf[e], pf[e + 1]};
+                const bf16x2_t pair = {pf[t][e], pf[t][e + 1]};
                 l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
-            }
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const int d = 32 * mt + qc;
-                const int pch = half ^ ((d >> 3) & 1);
-                const bf16x8 a =
-                    as_bf16x8(*reinterpret_cast<const u32x4 *>(tv + ((t * D + d) * 2 + pch) * 16));
-                o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, o_acc[mt], 0, 0, 0);
             }
         }
     };
 
-    const int last_tile = ntiles - 1;
-    const bool last_needs_zero = (last_tile + 1) * kTileKeys > total;
-    const int last_owner = last_tile >= split ? 1 : 0;
-    const int last_iter = last_tile - (last_owner ? split : 0);
+    // Ping-pong schedule. Each group runs the cluster sequence
+    //   C(-1), M(0), C(0), M(1), C(1), ..., M(n-1), C(n-1)
+    // with C(j) = [PV(j), QK(j+1)] (matrix) and M(j) = [softmax(j), loads of V(j+1)
+    // and K(j+2)] (vector). Group 1 runs one phase behind group 0, so in every phase
+    // each SIMD has one wave in a matrix cluster and one in a vector cluster. Every
+    // phase ends with a workgroup barrier (both groups pass the same number); the
+    // loads issued in M(j) are waited for at the end of M(j+1), one phase before
+    // C(j+1) reads them. Rows whose causal limit ends before a tile get P = 0 there.
+    // Block ids travel one phase ahead: at C(j), ids_v holds tile j+1's (for V(j+1))
+    // and ids_k tile j+2's (for K(j+2)).
+    int32_t ids_v[kTileBlocks], ids_k[kTileBlocks], ids_raw[kTileBlocks];
+    tile_ids(0, ids_v);
+    if (n > 0) issue_k(0, ids_v);                      // K(0) for C(-1)
+    tile_ids(1, ids_k);
+    wait_vmem();
+    __syncthreads();
 
-    int32_t ids[kTileBlocks];
-    if (tile_begin < tile_end) {
-        tile_ids(tile_begin, ids);
-        issue_tile(ids, 0);
-        if (tile_begin + 1 < tile_end) tile_ids(tile_begin + 1, ids);
-    }
-
-    for (int it = 0; it < niter; ++it) {
-        const int buf = it & 1;
-        const int kt = tile_begin + it;
-        const bool have = kt < tile_end;
+    const int n0 = split, n1 = ntiles - split;
+    const int phases = max(2 * n0 + 1, 2 * n1 + 2);
+    int ph = 0;
+    auto phase_end = [&]() {
+        phase_barrier();
+        ++ph;
+    };
+    // M(j): softmax of tile j; block ids of tile j+2 (read now, range-checked at the
+    // end, when they have long arrived); then wait for the loads C(j-1) issued.
+    auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+        tile_ids(j + 2, ids_raw);
+        softmax(j, st, pf);
+#pragma unroll
+        for (int jb = 0; jb < kTileBlocks; ++jb) {
+            ids_v[jb] = ids_k[jb];
+            ids_k[jb] = checked(ids_raw[jb]);
+        }
         wait_vmem();
-        __syncthreads();
-        if (last_needs_zero && it == last_iter) {                  // uniform over the workgroup
-            if (grp == last_owner) zero_tail(kt, buf);
-            __syncthreads();
+    };
+
+    f32x16 st[2];
+    bf16x8 pf[kTileBlocks];
+    if (grp == 1) phase_end();
+    if (n > 0) {
+        // C(-1): QK(0), loads of V(0) and K(1) (K(1) lands in an unused buffer if n == 1)
+        matrix_cluster(std::false_type{}, std::true_type{}, -1, pf, st, ids_v, ids_k);
+        phase_end();
+        for (int j = 0; j + 1 < n; ++j) {
+            vector_cluster(j, st, pf);
+            phase_end();
+            // C(j): PV(j), QK(j+1), loads of V(j+1) and K(j+2) (the last K lands unused)
+            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k);
+            phase_end();
         }
-        if (have && kt + 1 < tile_end) {
-            issue_tile(ids, buf ^ 1);                              // ids of tile kt+1
-            if (kt + 2 < tile_end) tile_ids(kt + 2, ids);
-        }
-        if (!have || kt * kTileKeys > w_max_limit) continue;
-        compute_tile(kt * kTileKeys + kTileKeys - 1 > w_min_limit, kt, buf);
+        vector_cluster(n - 1, st, pf);
+        phase_end();
+        // The group's last tile may hold the sequence end: clear V past it.
+        if ((tile_begin + n) * kTileKeys > total) pv(n - 1, pf, std::true_type{});
+        else matrix_cluster(std::true_type{}, std::false_type{}, n - 1, pf, st, ids_v, ids_k);
+        phase_end();
     }
+    while (ph < phases) phase_end();
 
     // ---- merge the two key halves through LDS, normalise, store ----
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     __syncthreads();
-    float *xch = reinterpret_cast<float *>(&lds[0][0][0]);
+    float *xch = reinterpret_cast<float *>(&lds[0][0]);
     constexpr int XW = 4 * MT + 1;                 // float4 slots per lane: O, then (m, l)
     if (grp == 1) {
         f32x4 *x4 = reinterpret_cast<f32x4 *>(xch) + (size_t)wg * XW * 64;
@@ -352,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 for (int c = 0; c < 4; ++c) v[c] = o_acc[mt][4 * r4 + c];
                 x4[(mt * 4 + r4) * 64 + lane] = v;
             }
-        f32x4 ml = {m_run, l_tot, 0.f, 0.f};
+        f32x4 ml = {has_ref ? m_ref : -INFINITY, l_tot, 0.f, 0.f};
         x4[(XW - 1) * 64 + lane] = ml;
     }
     __syncthreads();
@@ -361,8 +501,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const f32x4 *x4 = reinterpret_cast<const f32x4 *>(xch) + (size_t)wg * XW * 64;
     const f32x4 ml = x4[(XW - 1) * 64 + lane];
     const float m1 = ml[0], l1 = ml[1];
-    const float mm = fmaxf(m_run, m1);
-    const float a0 = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+    const float m0 = has_ref ? m_ref : -INFINITY;
+    const float mm = fmaxf(m0, m1);
+    const float a0 = (m0 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m0 - mm);
     const float a1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
     const float inv = 1.f / (a0 * l_tot + a1 * l1);
     if (row_valid && tq < T) {
