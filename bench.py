@@ -38,6 +38,44 @@ if ROOT not in sys.path:
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16
 HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
+ATTN_SOURCE = os.path.join(ROOT, "paper_2603_23049_amd", "csrc", "attn.hip")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "prefill_attn_l8b_layer_traffic.md")
+
+
+def source_sha256(path: str) -> str:
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary, or None when
+    the summary is missing or was taken on a different attention source."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_PROFILE):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("attn_source_sha256") != source_sha256(ATTN_SOURCE):
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(nbytes=256 << 20, reps=5):
+    """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read_per_launch": nbytes, "copy_bytes_written_per_launch": nbytes,
+                      "launches": reps}), flush=True)
 
 
 def attention_flops(prefix_lens, suffix_lens, num_q_heads, head_dim) -> float:
@@ -106,7 +144,8 @@ def _attn(L, bp, stream=None):
 
 
 def measure_step(batch, steps, warmup):
-    """Timed compute step (append + attention) with prefix KV already in the pool."""
+    """Timed compute step (append + attention) with prefix KV already in the pool; then
+    the attention and append kernels alone, back to back, for their per-launch time."""
     import torch
     from paper_2603_23049_amd import pcr
     L, bp, _ = _setup_layer(batch)
@@ -117,22 +156,30 @@ def measure_step(batch, steps, warmup):
         pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
         _attn(L, bp, s)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
-    for a, m, e in ev:
+    for a, e in ev:
         a.record(s)
         pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
-        m.record(s)
         _attn(L, bp, s)
         e.record(s)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_ms = [a.elapsed_time(e) for a, m, e in ev]
-    append_ms = [a.elapsed_time(m) for a, m, e in ev]
-    attn_ms = [m.elapsed_time(e) for a, m, e in ev]
-    return dict(step_ms=float(np.mean(step_ms)), append_ms=float(np.mean(append_ms)),
-                attn_ms=float(np.mean(attn_ms)), attn_ms_median=_median(attn_ms), wall_s=wall)
+    step_ms = [a.elapsed_time(e) for a, e in ev]
+
+    def back_to_back(fn):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(steps):
+            fn()
+        e.record(s)
+        e.synchronize()
+        return a.elapsed_time(e) / steps
+
+    attn_ms = back_to_back(lambda: _attn(L, bp, s))
+    append_ms = back_to_back(lambda: pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s))
+    return dict(step_ms=float(np.mean(step_ms)), step_ms_median=_median(step_ms), append_ms=append_ms,
+                attn_ms=attn_ms, wall_s=wall)
 
 
 def measure_load(batch, reps=10):
@@ -177,8 +224,10 @@ def measure_load(batch, reps=10):
     return out
 
 
-def measure_pipeline(batch, method, reps=3):
-    """The n-layer two-stream pipeline; exposure per layer measured and bounded."""
+def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3):
+    """The n-layer two-stream pipeline. Exposure per layer is the pipeline's time per
+    layer beyond the layer's isolated compute; its least possible value follows from
+    the isolated per-layer load and compute times (two in-order queues)."""
     import torch
     from paper_2603_23049_amd import pcr
     n = batch.num_layers
@@ -195,21 +244,25 @@ def measure_pipeline(batch, method, reps=3):
         if r >= 1:
             runs.append(t)
     best = min(runs, key=lambda t: t["total_ms"])
-    load_ms = float(np.median(best["load_ms"][1:])) if n > 1 else float(best["load_ms"][0])
-    comp_ms = float(np.median(best["compute_ms"]))
-    e_raw = (best["total_ms"] - best["sum_compute_ms"]) / n
-    e_min = flow_shop_exposure(load_ms, comp_ms, n) / n
-    return {"layers": n, "method": method, "total_ms": best["total_ms"], "sum_compute_ms": best["sum_compute_ms"],
-            "load_ms_per_layer": load_ms, "compute_ms_per_layer": comp_ms,
+    e_raw = best["total_ms"] / n - compute_ms_iso
+    e_min = flow_shop_exposure(load_ms_iso, compute_ms_iso, n) / n
+    del layers
+    torch.cuda.synchronize()
+    return {"layers": n, "workload": batch.name, "method": method, "total_ms": best["total_ms"],
+            "sum_compute_ms_in_pipeline": best["sum_compute_ms"],
+            "load_ms_per_layer_isolated": load_ms_iso, "compute_ms_per_layer_isolated": compute_ms_iso,
+            "load_ms_per_layer_in_pipeline": float(np.median(best["load_ms"])),
+            "compute_ms_per_layer_in_pipeline": float(np.median(best["compute_ms"])),
             "exposed_ms_per_layer": e_raw, "exposed_min_ms_per_layer": e_min,
             "exposed_over_min_ms_per_layer": e_raw - e_min,
-            "exposed_over_min_frac_of_load": (e_raw - e_min) / load_ms if load_ms > 0 else None,
-            "exposed_frac_of_load": e_raw / load_ms if load_ms > 0 else None}
+            "exposed_over_min_frac_of_load": (e_raw - e_min) / load_ms_iso if load_ms_iso > 0 else None,
+            "exposed_frac_of_load": e_raw / load_ms_iso if load_ms_iso > 0 else None,
+            "bound_makespan_ms": flow_shop_exposure(load_ms_iso, compute_ms_iso, n) + n * compute_ms_iso}
 
 
-def cpu_baseline(batch, budget_s=15.0):
-    """The fp64 oracle on a bounded sample of the layer: every head of an evenly spread
-    subset of the suffix tokens, scaled to TFLOP/s by the sample's causal-exact FLOPs."""
+def cpu_baseline(batch, budget_s=12.0):
+    """The fp64 oracle (as it stands) on the same layer, repeated until about budget_s
+    of CPU time has passed; TFLOP/s by the layer's causal-exact FLOPs."""
     from oracle import attention as oattn
     from oracle import datamove as odm
     from paper_2603_23049_amd import synth
@@ -218,30 +271,17 @@ def cpu_baseline(batch, budget_s=15.0):
     shape = (batch.pool_blocks, batch.num_kv_heads, 16 * batch.head_dim)
     pk, pv = odm.pool_after_layer(np.zeros(shape, np.uint16), np.zeros(shape, np.uint16), data.host_k, data.host_v,
                                   plan, data.k_new, data.v_new)
-    cu = plan[3]
-    Hq, d = batch.num_q_heads, batch.head_dim
-
-    def flops_of(rows):
-        f = 0
-        for t, _ in rows:
-            b = int(np.searchsorted(cu, t, side="right") - 1)
-            f += 4 * d * (batch.prefix_lens[b] + (t - cu[b]) + 1)
-        return float(f)
-
-    stride = 64
+    flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
+    reps, t0 = 0, time.perf_counter()
     while True:
-        toks = list(range(0, batch.T, stride))
-        rows = np.array([[t, h] for t in toks for h in range(Hq)], np.int32)
-        t0 = time.perf_counter()
-        oattn.attention(data.q, pk, pv, batch.block_tables, np.asarray(batch.prefix_lens, np.int32), cu,
-                        batch.num_kv_heads, 16, rows=rows)
+        oattn.attention(data.q, pk, pv, batch.block_tables, np.asarray(batch.prefix_lens, np.int32), plan[3],
+                        batch.num_kv_heads, 16)
+        reps += 1
         dt = time.perf_counter() - t0
-        if dt * 2 >= budget_s or stride == 1:
+        if dt >= budget_s:
             break
-        stride = max(1, int(stride * dt / budget_s * 1.5) or 1)
-    return {"value": flops_of(rows) / dt / 1e12, "unit": "TFLOP/s", "cores": oattn.num_threads(), "kind": "oracle",
-            "sample": f"every head of every {stride}th suffix token of the layer ({len(rows)} of "
-                      f"{batch.T * Hq} rows), fp64, {dt:.1f} s"}
+    return {"value": reps * flops / dt / 1e12, "unit": "TFLOP/s", "cores": oattn.num_threads(), "kind": "oracle",
+            "sample": f"the whole {batch.name} layer (every row of every head), fp64, {reps} passes in {dt:.1f} s"}
 
 
 def main(argv=None):
@@ -254,6 +294,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-load", action="store_true", help="skip the host-to-pool copy measurements")
     ap.add_argument("--pipeline-method", default="auto")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 256 MiB device copy (reference for the traffic counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -267,6 +309,9 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     pcr.lib()   # fails loudly if libpcr.so is missing
+    if args.copy_calibration:
+        copy_calibration()
+        return 0
 
     batch = synth.REGISTRY[args.workload]()
     flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
@@ -283,9 +328,12 @@ def main(argv=None):
         load = measure_load(batch)
     pipe = None
     if not args.no_pipeline:
+        if load is None:
+            load = measure_load(batch)
         pbatch = synth.l8b_pipe32()
+        method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
         _say(f"[bench] pipeline: {pbatch.name} ({pbatch.num_layers} layers)")
-        pipe = measure_pipeline(pbatch, args.pipeline_method)
+        pipe = measure_pipeline(pbatch, args.pipeline_method, load[method]["ms"], st["step_ms"])
     cpu = None
     if not args.no_cpu_baseline:
         _say("[bench] cpu baseline (oracle)")
@@ -312,7 +360,7 @@ def main(argv=None):
         "mfma_frac": value / MFMA_BF16_PEAK_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": "prefill_attn_kernel", "achieved": attn_tflops,
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
-                     "traffic": None, "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"]},
+                     "traffic": measured_traffic(), "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"]},
         "append": {"ms": st["append_ms"], "bytes": app_b, "GBps": app_b / st["append_ms"] / 1e6,
                    "frac_hbm": app_b / st["append_ms"] / 1e6 / HBM_PEAK_GBS},
         "load": load,

@@ -148,6 +148,10 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(
 // before their stores. Grid-stride over the 2*n block copies.
 // ---------------------------------------------------------------------------
 constexpr int kPullUnroll = 8;
+// Workgroups of one pull launch: 32 x 256 lanes x 8 x 16 B = 1 MiB in flight, enough
+// to saturate a PCIe 5 x16 host link while leaving the other CUs to the compute stream
+// (on MI355X, 16 workgroups reach about 85% of the link, 32 and more the full link).
+constexpr int kPullWorkgroups = 32;
 
 __global__ __launch_bounds__(256) void pull_blocks_kernel(
     const u32x4 *__restrict__ host_k, const u32x4 *__restrict__ host_v, int64_t host_blocks,
@@ -221,7 +225,7 @@ hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t ho
 {
     if (args.n <= 0) return hipSuccess;
     const int units = 2 * args.n;
-    const int grid = units < 64 ? units : 64;
+    const int grid = units < kPullWorkgroups ? units : kPullWorkgroups;
     hipLaunchKernelGGL(pull_blocks_kernel, dim3(grid), dim3(256), 0, s,
                        static_cast<const u32x4 *>(host_k), static_cast<const u32x4 *>(host_v),
                        host_blocks, static_cast<u32x4 *>(pool_k), static_cast<u32x4 *>(pool_v),
