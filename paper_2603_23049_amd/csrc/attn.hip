@@ -59,6 +59,9 @@ constexpr int kTileKeys = 64;
 constexpr int kTileBlocks = kTileKeys / kBlockSize;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleThreshold = 8.0f;                // log2 units
+#ifndef KAHEAD
+#define KAHEAD 8
+#endif
 constexpr int kXcds = 8;                                 // MI355X: 8 XCDs, workgroups dealt round-robin
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -94,9 +97,27 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // keep the compiler from moving memory operations across the barrier.
 __device__ __forceinline__ void phase_barrier()
 {
+    __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// One wave-wide direct load global -> LDS: lane l's 16 bytes at src land at
+// lds_dst + 16*l (lds_dst wave-uniform). Issued as inline assembly because the
+// compiler counts a global-to-LDS load as a pending LDS access of unknown order and
+// then drains every outstanding LDS read (lgkmcnt(0)) at the next operand wait,
+// which would empty the fragment pipeline after each load. The hardware signals
+// completion of these loads on vmcnt only; the kernel waits for them explicitly
+// before the barrier that precedes their first reader.
+// The source is a wave-uniform base (SGPR pair) plus a 32-bit per-lane byte offset.
+// lds_dst is an LDS byte address (M0 form).
+__device__ __forceinline__ void dma16(const char *base, uint32_t lane_off, uint32_t lds_dst)
+{
+    const unsigned m0 = __builtin_amdgcn_readfirstlane(lds_dst);
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(base), "s"(m0)
+                 : "memory", "m0");
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding
@@ -119,7 +140,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     constexpr int CPR = Geo::CPR;
     constexpr int KSTEPS = D / 16;
     constexpr int MT = D / 32;
-    constexpr int64_t kHeadPayload = kBlockSize * D;
+    constexpr int64_t kPayloadBytes = kBlockSize * D * 2;   // one (block, kv head) of K or V
+    constexpr int kSlabs = (int)(kPayloadBytes / 1024);       // 1 KB slabs per payload
+    static_assert(kGroupWaves % kSlabs == 0, "slab-to-wave mapping");
     constexpr int kKLoads = Geo::KLOADS, kVLoads = Geo::VLOADS;
 
     // Per group: K buffers 0/1 then V buffers 0/1 (double-buffered, tile j in buffer j&1);
@@ -205,6 +228,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int32_t *bt = block_tables + (int64_t)b * max_blocks;
     auto kbuf = [&](int j) { return &lds[grp][(j & 1) * Geo::KBYTES]; };
     auto vbuf = [&](int j) { return &lds[grp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
+    // The same buffers as LDS byte addresses, for the direct loads (no generic-pointer casts).
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)&lds[grp][0];
+    auto kbuf_off = [&](int j) { return (uint32_t)((j & 1) * Geo::KBYTES); };
+    auto vbuf_off = [&](int j) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
 
     // Pool block ids of this group's tile j, read raw (as scalars) one phase before
     // use; logical blocks past the sequence read nothing. The range check happens at
@@ -218,41 +245,47 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             ids[jb] = lb < valid_blocks ? bt[lb] : 0;
         }
     };
-    auto checked = [&](int32_t blk) { return (blk < 0 || blk >= num_blocks) ? 0 : blk; };
+    // Byte offset of the (pool block, kv head g) payload of a raw block id; an id outside
+    // the pool becomes block 0. (blk * Hkv + g fits in 32 bits for any pool that fits in
+    // memory: 2^32 payloads would be 8 TB.)
+    auto payload_off = [&](int32_t blk) -> int64_t {
+        const uint32_t b = (uint32_t)blk < (uint32_t)num_blocks ? (uint32_t)blk : 0u;
+        return (int64_t)(b * (uint32_t)Hkv + (uint32_t)g) * kPayloadBytes;
+    };
+    auto to_offs = [&](const int32_t (&ids)[kTileBlocks], int64_t (&offs)[kTileBlocks]) {
+#pragma unroll
+        for (int jb = 0; jb < kTileBlocks; ++jb) offs[jb] = payload_off(ids[jb]);
+    };
+    // Direct-load addressing. A tile's K (or V) is 4 pool blocks of one kv head, each a
+    // contiguous payload of kSlabs 1 KB slabs; wave wg loads slabs u*4 + wg. Because 4
+    // is a multiple of kSlabs, a lane's byte offset inside the payload is the same for
+    // every u, so it is computed once here; the LDS swizzle is applied through it.
+    const char *pool_k_bytes = reinterpret_cast<const char *>(pool_k);
+    const char *pool_v_bytes = reinterpret_cast<const char *>(pool_v);
+    uint32_t k_off, v_off;
+    {
+        const int chunk = (wg % kSlabs) * 64 + lane;          // 16-B chunk within the payload
+        const int key = chunk / CPR, pc = chunk % CPR;        // K: row (slot) and chunk of the row
+        k_off = (uint32_t)(key * 2 * D + ((pc ^ k_swizzle<CPR>(key)) * 16));
+        const int d = chunk >> 1, pch = chunk & 1;            // V: dim and half of its 16 slots
+        v_off = (uint32_t)(d * 2 * kBlockSize + ((pch ^ ((d >> 3) & 1)) * 16));
+    }
 
     // Direct loads of this group's tile j (K or V) into its buffer; 1 KB slab per
     // wave-wide load; the LDS swizzle is applied through each lane's source.
     // One direct load (load u of the tile's K or V) of this group's tile j into its buffer:
     // a 1 KB slab per wave-wide load; the LDS swizzle is applied through each lane's source.
-    auto load_k = [&](int j, const int32_t (&ids)[kTileBlocks], int u) {
+    auto load_k = [&](int j, const int64_t (&offs)[kTileBlocks], int u) {
         const int slab = u * kGroupWaves + wg;                             // wave-uniform
-        const int jb = (slab * 64) / (CPR * kBlockSize);                   // pool block of the slab
-        const int P = slab * 64 + lane;
-        const int key = P / CPR, pc = P % CPR;
-        const int c = pc ^ k_swizzle<CPR>(key);
-        const int64_t head_base = ((int64_t)checked(ids[jb]) * Hkv + g) * kHeadPayload;
-        const u16 *src = pool_k + head_base + (key % kBlockSize) * D + c * 8;
-        __builtin_amdgcn_global_load_lds(
-            (const void *)src, (__attribute__((address_space(3))) void *)(kbuf(j) + slab * 1024), 16, 0, 0);
+        dma16(pool_k_bytes + offs[slab / kSlabs], k_off, lds_addr + kbuf_off(j) + slab * 1024);
     };
-    auto load_v = [&](int j, const int32_t (&ids)[kTileBlocks], int u) {
+    auto load_v = [&](int j, const int64_t (&offs)[kTileBlocks], int u) {
         const int slab = u * kGroupWaves + wg;
-        const int jb = (slab * 64) / (2 * D);
-        const int within = (slab * 64 + lane) % (2 * D);
-        const int d = within >> 1, pch = within & 1;
-        const int ch = pch ^ ((d >> 3) & 1);
-        const int64_t head_base = ((int64_t)checked(ids[jb]) * Hkv + g) * kHeadPayload;
-        const u16 *src = pool_v + head_base + d * kBlockSize + ch * 8;
-        __builtin_amdgcn_global_load_lds(
-            (const void *)src, (__attribute__((address_space(3))) void *)(vbuf(j) + slab * 1024), 16, 0, 0);
+        dma16(pool_v_bytes + offs[slab / kSlabs], v_off, lds_addr + vbuf_off(j) + slab * 1024);
     };
-    auto issue_k = [&](int j, const int32_t (&ids)[kTileBlocks]) {
+    auto issue_k = [&](int j, const int64_t (&offs)[kTileBlocks]) {
 #pragma unroll
-        for (int u = 0; u < kKLoads; ++u) load_k(j, ids, u);
-    };
-    auto issue_v = [&](int j, const int32_t (&ids)[kTileBlocks]) {
-#pragma unroll
-        for (int u = 0; u < kVLoads; ++u) load_v(j, ids, u);
+        for (int u = 0; u < kKLoads; ++u) load_k(j, offs, u);
     };
 
     // ---- matrix work: S^T(j) = K(j) Q^T over two 32-key halves ----
@@ -301,13 +334,13 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // behind the MFMAs). When QK runs, the cluster also issues the direct loads of
     // V(j+1) and K(j+2), one per few MFMAs, so the texture path never backs up a wave.
     auto matrix_cluster = [&](auto pv_tag, auto qk_tag, int j, const bf16x8 (&pf)[kTileBlocks],
-                              f32x16 (&st)[2], const int32_t (&idv)[kTileBlocks],
-                              const int32_t (&idk)[kTileBlocks]) {
+                              f32x16 (&st)[2], const int64_t (&idv)[kTileBlocks],
+                              const int64_t (&idk)[kTileBlocks]) {
         constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
         constexpr int NPV = DO_PV ? kTileBlocks * MT : 0, NQK = DO_QK ? 2 * KSTEPS : 0, NALL = NPV + NQK;
         constexpr int NLD = DO_QK ? kVLoads + kKLoads : 0;
         constexpr int EVERY = NLD ? (NALL / NLD > 0 ? NALL / NLD : 1) : 1;
-        constexpr int kAhead = 4;
+        constexpr int kAhead = KAHEAD;
         const char *tv = vbuf(j);
         const char *tk = kbuf(j + 1);
         auto frag = [&](int i) -> u32x4 {
@@ -346,15 +379,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         // keep that schedule: the first reads, then (read, MFMA[, load]) groups, then the last MFMAs
 #pragma unroll
         for (int i = 0; i < kAhead && i < NALL; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        int ld2 = 0;
 #pragma unroll
         for (int i = 0; i < NALL; ++i) {
             if (i + kAhead < NALL) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (NLD && i % EVERY == EVERY - 1 && ld2 < NLD) {
-                __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-                ++ld2;
-            }
         }
     };
 
@@ -370,15 +398,18 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 for (int r = 0; r < 16; ++r)
                     st[m][r] = (32 * m + 16 * (r >> 3) + (r & 7)) > lim ? -INFINITY : st[m][r];
         }
+        // NaN-propagating maximum (v_maximum3_f32): unlike fmaxf it needs no
+        // canonicalisation of the MFMA results, one instruction per two scores.
         float mx = -INFINITY;
 #pragma unroll
         for (int m = 0; m < 2; ++m)
 #pragma unroll
-            for (int r = 0; r < 16; r += 2) mx = fmaxf(mx, fmaxf(st[m][r], st[m][r + 1]));
+            for (int r = 0; r < 16; r += 2)
+                mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(st[m][r], st[m][r + 1]));
         {   // the other half-wave holds the other 32 keys of the same query
             const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
                                                              __builtin_bit_cast(unsigned, mx), false, false);
-            mx = fmaxf(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+            mx = __builtin_elementwise_maximum(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
         }
         // Move the reference up when the tile's max exceeds it by more than 2^8, or set it
         // from the first real score; keeps P <= 256 without rescaling O on most tiles.
@@ -426,10 +457,13 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // C(j+1) reads them. Rows whose causal limit ends before a tile get P = 0 there.
     // Block ids travel one phase ahead: at C(j), ids_v holds tile j+1's (for V(j+1))
     // and ids_k tile j+2's (for K(j+2)).
-    int32_t ids_v[kTileBlocks], ids_k[kTileBlocks], ids_raw[kTileBlocks];
-    tile_ids(0, ids_v);
+    int64_t ids_v[kTileBlocks], ids_k[kTileBlocks];   // payload byte offsets
+    int32_t ids_raw[kTileBlocks];
+    tile_ids(0, ids_raw);
+    to_offs(ids_raw, ids_v);
     if (n > 0) issue_k(0, ids_v);                      // K(0) for C(-1)
-    tile_ids(1, ids_k);
+    tile_ids(1, ids_raw);
+    to_offs(ids_raw, ids_k);
     wait_vmem();
     __syncthreads();
 
@@ -448,7 +482,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) {
             ids_v[jb] = ids_k[jb];
-            ids_k[jb] = checked(ids_raw[jb]);
+            ids_k[jb] = payload_off(ids_raw[jb]);
         }
         wait_vmem();
     };
