@@ -189,7 +189,6 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int tile_begin = grp ? split : 0;
     const int n = (grp ? ntiles : split) - tile_begin;   // this group's tiles
     const int w_first = min(rows_total - 1, row0 + wg * kRowsPerWave);
-    const int w_last = min(rows_total - 1, row0 + wg * kRowsPerWave + kRowsPerWave - 1);
     const int w_min_limit = p + w_first / G;
     const int valid_blocks = min((total + kBlockSize - 1) / kBlockSize, max_blocks);
 
@@ -219,8 +218,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // Scores are kept relative to a reference m_ref (log2 domain): the first product
     // starts from -m_ref, so S^T holds scale*log2(e)*<q,k> - m_ref and P = exp2(S^T).
     float m_ref = 0.f;
-    bool has_ref = false;      // m_ref has been set from a real score
-    float l_run = 0.f;         // this lane's part of the denominator
+    // The reference moves when a tile's max (relative to it) exceeds thr: -inf until the
+    // first real score of the row, then 2^8, so P stays <= 256 and O is rescaled rarely.
+    float thr = -INFINITY;
+    float l_run[2] = {0.f, 0.f};   // this lane's part of the denominator (two chains)
     f32x16 nbias;
 #pragma unroll
     for (int r = 0; r < 16; ++r) nbias[r] = 0.f;
@@ -234,15 +235,17 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     auto vbuf_off = [&](int j) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
 
     // Pool block ids of this group's tile j, read raw (as scalars) one phase before
-    // use; logical blocks past the sequence read nothing. The range check happens at
-    // use, so the scalar loads are never waited for on the spot: an id past the
-    // sequence or outside the pool becomes block 0 (its keys are masked and its V
-    // entries cleared before use), so no load ever leaves the pool.
+    // use. Logical blocks past the sequence read the last valid entry (so the loads
+    // need no branch) and become block 0. The range check happens at use, so the
+    // scalar loads are never waited for on the spot: an id past the sequence or
+    // outside the pool becomes block 0 (its keys are masked and its V entries cleared
+    // before use), so no load ever leaves the pool.
     auto tile_ids = [&](int j, int32_t (&ids)[kTileBlocks]) {
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) {
             const int lb = (tile_begin + j) * kTileBlocks + jb;
-            ids[jb] = lb < valid_blocks ? bt[lb] : 0;
+            const int32_t v = bt[min(lb, valid_blocks - 1)];
+            ids[jb] = lb < valid_blocks ? v : 0;
         }
     };
     // Byte offset of the (pool block, kv head g) payload of a raw block id; an id outside
@@ -286,21 +289,6 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     auto issue_k = [&](int j, const int64_t (&offs)[kTileBlocks]) {
 #pragma unroll
         for (int u = 0; u < kKLoads; ++u) load_k(j, offs, u);
-    };
-
-    // ---- matrix work: S^T(j) = K(j) Q^T over two 32-key halves ----
-    auto qk = [&](int j, f32x16 (&st)[2]) {
-        const char *tk = kbuf(j);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const int krow = 32 * m + key_of_row(qc);
-#pragma unroll
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-                const int pc = (2 * ks + half) ^ k_swizzle<CPR>(krow);
-                const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(tk + (krow * CPR + pc) * 16));
-                st[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], ks == 0 ? nbias : st[m], 0, 0, 0);
-            }
-        }
     };
 
     // ---- matrix work: O^T += V^T(j) P^T(j), k-step t = pool block t of the tile.
@@ -355,6 +343,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             const int pc = (2 * ks + half) ^ k_swizzle<CPR>(krow);
             return *reinterpret_cast<const u32x4 *>(tk + (krow * CPR + pc) * 16);
         };
+        // The wave in its matrix cluster takes issue priority over the other wave of its
+        // SIMD (in its vector cluster): otherwise the older wave of each SIMD always wins
+        // arbitration and the younger group is late in every phase.
+        __builtin_amdgcn_s_setprio(1);
         u32x4 fr[NALL];
 #pragma unroll
         for (int i = 0; i < kAhead && i < NALL; ++i) fr[i] = frag(i);
@@ -384,6 +376,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             if (i + kAhead < NALL) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
     };
 
     // ---- vector work: online softmax of S^T(j) into bf16 P(j) (log2 domain, lazy rescale) ----
@@ -411,15 +405,14 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                                                              __builtin_bit_cast(unsigned, mx), false, false);
             mx = __builtin_elementwise_maximum(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
         }
-        // Move the reference up when the tile's max exceeds it by more than 2^8, or set it
-        // from the first real score; keeps P <= 256 without rescaling O on most tiles.
-        const bool need = (mx > kRescaleThreshold) || (!has_ref && mx > -INFINITY);
+        const bool need = mx > thr;
         if (__builtin_amdgcn_ballot_w64(need)) {
             const float delta = need ? mx : 0.f;
             const float alpha = __builtin_amdgcn_exp2f(-delta);
-            has_ref = has_ref || need;
+            thr = need ? kRescaleThreshold : thr;
             m_ref += delta;
-            l_run *= alpha;
+            l_run[0] *= alpha;
+            l_run[1] *= alpha;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -431,7 +424,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) nbias[r] = -m_ref;
         }
-        const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+        // Row sums from the fp32 probabilities with plain adds: the bf16 dot instructions
+        // would serve the same purpose in half the count, but they wait behind the other
+        // wave's MFMAs on this SIMD (measured about 70 cycles each), while VALU adds issue
+        // beside them.
 #pragma unroll
         for (int t = 0; t < kTileBlocks; ++t) {
             f32x8 pv8;
@@ -439,24 +435,21 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             for (int e = 0; e < 8; ++e)
                 pv8[e] = __builtin_amdgcn_exp2f(st[t >> 1][8 * (t & 1) + e]);
             pf[t] = __builtin_convertvector(pv8, bf16x8);
-#pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const bf16x2_t pair = {pf[t][e], pf[t][e + 1]};
-                l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
-            }
+            l_run[0] += (pv8[0] + pv8[1]) + (pv8[2] + pv8[3]);
+            l_run[1] += (pv8[4] + pv8[5]) + (pv8[6] + pv8[7]);
         }
     };
 
     // Ping-pong schedule. Each group runs the cluster sequence
     //   C(-1), M(0), C(0), M(1), C(1), ..., M(n-1), C(n-1)
-    // with C(j) = [PV(j), QK(j+1)] (matrix) and M(j) = [softmax(j), loads of V(j+1)
-    // and K(j+2)] (vector). Group 1 runs one phase behind group 0, so in every phase
-    // each SIMD has one wave in a matrix cluster and one in a vector cluster. Every
-    // phase ends with a workgroup barrier (both groups pass the same number); the
-    // loads issued in M(j) are waited for at the end of M(j+1), one phase before
+    // with C(j) = [PV(j), QK(j+1), direct loads of V(j+1) and K(j+2)] (matrix) and
+    // M(j) = [softmax(j)] (vector). Group 1 runs one phase behind group 0, so in every
+    // phase each SIMD has one wave in a matrix cluster and one in a vector cluster.
+    // Every phase ends with a workgroup barrier (both groups pass the same number);
+    // the loads issued in C(j) are waited for at the end of M(j+1), one phase before
     // C(j+1) reads them. Rows whose causal limit ends before a tile get P = 0 there.
-    // Block ids travel one phase ahead: at C(j), ids_v holds tile j+1's (for V(j+1))
-    // and ids_k tile j+2's (for K(j+2)).
+    // Block offsets travel one phase ahead: at C(j), ids_v holds tile j+1's (for
+    // V(j+1)) and ids_k tile j+2's (for K(j+2)).
     int64_t ids_v[kTileBlocks], ids_k[kTileBlocks];   // payload byte offsets
     int32_t ids_raw[kTileBlocks];
     tile_ids(0, ids_raw);
@@ -479,6 +472,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
         tile_ids(j + 2, ids_raw);
         softmax(j, st, pf);
+        __builtin_amdgcn_sched_barrier(0);   // the id conversion waits for the scalar loads: keep it last
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) {
             ids_v[jb] = ids_k[jb];
@@ -511,7 +505,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     while (ph < phases) phase_end();
 
     // ---- merge the two key halves through LDS, normalise, store ----
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_own = l_run[0] + l_run[1];
+    const float l_tot = l_own + __shfl_xor(l_own, 32);
+    const bool has_ref = thr > -INFINITY;      // this row saw a real score in this key half
     __syncthreads();
     float *xch = reinterpret_cast<float *>(&lds[0][0]);
     constexpr int XW = 4 * MT + 1;                 // float4 slots per lane: O, then (m, l)
