@@ -103,6 +103,16 @@ def flow_shop_exposure(load_ms: float, compute_ms: float, n: int) -> float:
     return makespan - n * compute_ms
 
 
+def workload(name):
+    """Named batch: the generator registry plus the RAG mix built through the prefix tree."""
+    from paper_2603_23049_amd import prefix_tree, synth
+    if name == "rag_mix":
+        return prefix_tree.rag_mix_batch()
+    if name == "l8b_pipe32_s6144":
+        return synth.l8b_pipe32(suffix=6144)
+    return synth.REGISTRY[name]()
+
+
 def _median(xs):
     return float(np.median(np.asarray(xs, dtype=np.float64)))
 
@@ -135,6 +145,27 @@ def _setup_layer(batch, layer=0, method="kernel_pull"):
     bp = pcr.BatchPlan(src, dst, dev(slots), dev(batch.block_tables), dev(pl), dev(cu), pl, cu,
                        batch.num_q_heads, 1.0 / math.sqrt(d))
     return L, bp, data
+
+
+def _setup_pipeline(batch, distinct):
+    """n layers with their own pools; host store, Q and new K/V come from `distinct`
+    generated layers used round-robin (same bytes moved and computed per layer)."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    base = []
+    bp = None
+    for l in range(min(distinct, batch.num_layers)):
+        L, bp_l, _ = _setup_layer(batch, l)
+        base.append(L)
+        bp = bp or bp_l
+    layers = list(base)
+    Hkv, d, bs = batch.num_kv_heads, batch.head_dim, batch.block_size
+    for l in range(len(base), batch.num_layers):
+        src = base[l % len(base)]
+        pool = pcr.KVPool(torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"),
+                          torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"), Hkv, d)
+        layers.append(pcr.Layer(src.host, pool, src.q, src.k_new, src.v_new, src.out))
+    return layers, bp
 
 
 def _attn(L, bp, stream=None):
@@ -224,19 +255,16 @@ def measure_load(batch, reps=10):
     return out
 
 
-def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3):
+def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinct=None):
     """The n-layer two-stream pipeline. Exposure per layer is the pipeline's time per
     layer beyond the layer's isolated compute; its least possible value follows from
-    the isolated per-layer load and compute times (two in-order queues)."""
+    the isolated per-layer load and compute times (two in-order queues). With
+    `distinct`, only that many layers' host/Q/K/V data are generated and reused
+    round-robin (every layer still has its own pool and moves its own bytes)."""
     import torch
     from paper_2603_23049_amd import pcr
     n = batch.num_layers
-    layers = []
-    bp = None
-    for l in range(n):
-        L, bp_l, _ = _setup_layer(batch, l)
-        layers.append(L)
-        bp = bp or bp_l
+    layers, bp = _setup_pipeline(batch, distinct or n)
     copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
     runs = []
     for r in range(reps + 1):
@@ -248,7 +276,8 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3):
     e_min = flow_shop_exposure(load_ms_iso, compute_ms_iso, n) / n
     del layers
     torch.cuda.synchronize()
-    return {"layers": n, "workload": batch.name, "method": method, "total_ms": best["total_ms"],
+    return {"layers": n, "workload": batch.name, "method": method, "distinct_layer_data": distinct or n,
+            "total_ms": best["total_ms"],
             "sum_compute_ms_in_pipeline": best["sum_compute_ms"],
             "load_ms_per_layer_isolated": load_ms_iso, "compute_ms_per_layer_isolated": compute_ms_iso,
             "load_ms_per_layer_in_pipeline": float(np.median(best["load_ms"])),
@@ -257,7 +286,8 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3):
             "exposed_over_min_ms_per_layer": e_raw - e_min,
             "exposed_over_min_frac_of_load": (e_raw - e_min) / load_ms_iso if load_ms_iso > 0 else None,
             "exposed_frac_of_load": e_raw / load_ms_iso if load_ms_iso > 0 else None,
-            "bound_makespan_ms": flow_shop_exposure(load_ms_iso, compute_ms_iso, n) + n * compute_ms_iso}
+            "bound_makespan_ms": flow_shop_exposure(load_ms_iso, compute_ms_iso, n) + n * compute_ms_iso,
+            "exposed_ideal_ms_per_layer": load_ms_iso / n if compute_ms_iso >= load_ms_iso else None}
 
 
 def cpu_baseline(batch, budget_s=12.0):
@@ -293,6 +323,8 @@ def main(argv=None):
     ap.add_argument("--no-pipeline", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-load", action="store_true", help="skip the host-to-pool copy measurements")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the RAG-mix attention line and the 80-layer and compute-bound pipelines")
     ap.add_argument("--pipeline-method", default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
@@ -313,7 +345,7 @@ def main(argv=None):
         copy_calibration()
         return 0
 
-    batch = synth.REGISTRY[args.workload]()
+    batch = workload(args.workload)
     flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
     _say(f"[bench] step: {args.workload} warmup={args.warmup} steps={args.steps}")
     st = measure_step(batch, args.steps, args.warmup)
@@ -327,13 +359,36 @@ def main(argv=None):
         _say("[bench] load")
         load = measure_load(batch)
     pipe = None
+    pipelines = {}
+    method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
     if not args.no_pipeline:
         if load is None:
             load = measure_load(batch)
         pbatch = synth.l8b_pipe32()
-        method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
         _say(f"[bench] pipeline: {pbatch.name} ({pbatch.num_layers} layers)")
         pipe = measure_pipeline(pbatch, args.pipeline_method, load[method]["ms"], st["step_ms"])
+        pipelines[pbatch.name] = pipe
+    extra = {}
+    if not args.no_extra:
+        rb = workload("rag_mix")
+        _say(f"[bench] rag_mix attention (T={rb.T})")
+        rst = measure_step(rb, max(10, args.steps // 2), 3)
+        rfl = attention_flops(rb.prefix_lens, rb.suffix_lens, rb.num_q_heads, rb.head_dim)
+        extra["rag_mix"] = {"attn_ms": rst["attn_ms"], "step_ms": rst["step_ms"], "flops": rfl,
+                            "attn_tflops": rfl / (rst["attn_ms"] * 1e-3) / 1e12,
+                            "frac": rfl / (rst["attn_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+                            "T": rb.T, "hit_ratio": rb.extra["hit_ratio"],
+                            "load_bytes": load_bytes(rb.prefix_lens, rb.num_kv_heads, rb.head_dim)}
+        if not args.no_pipeline:
+            for pb in (synth.l70b_pipe80(), synth.l8b_pipe32(suffix=6144)):
+                _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, 4 distinct layer data sets)")
+                pst = measure_step(pb, 10, 3)
+                pld = measure_load(pb, reps=4)
+                pipelines[pb.name] = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"],
+                                                      reps=2, distinct=4)
+                pipelines[pb.name]["attn_tflops"] = attention_flops(
+                    pb.prefix_lens, pb.suffix_lens, pb.num_q_heads, pb.head_dim) / (pst["attn_ms"] * 1e-3) / 1e12
+                pipelines[pb.name]["load_GBps"] = pld[method]["GBps"]
     cpu = None
     if not args.no_cpu_baseline:
         _say("[bench] cpu baseline (oracle)")
@@ -365,6 +420,8 @@ def main(argv=None):
                    "frac_hbm": app_b / st["append_ms"] / 1e6 / HBM_PEAK_GBS},
         "load": load,
         "pipeline": pipe,
+        "pipelines": pipelines or None,
+        "rag_mix": extra.get("rag_mix"),
         "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
         "cpu_baseline": cpu,
         "wall_s_timed": st["wall_s"],

@@ -34,6 +34,7 @@
 // XOR-swizzled so that lanes reading 32 different key rows (K) or dims (V)
 // hit distinct banks; the swizzle is applied through the source address of
 // each lane, since a direct load writes lane l's 16 bytes at base + 16*l.
+#include <algorithm>
 #include <type_traits>
 
 #include "pcr_internal.h"
@@ -129,12 +130,25 @@ __device__ __forceinline__ void wait_vmem_keep()
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Order of one launch's work items (row tile of a sequence, kv head), built on the
+// host from the sequence lengths and passed by value in the kernel arguments.
+// Sequences are taken heaviest first (longest key range), and inside a sequence the
+// last row tiles (the most keys) first, so the long items start early and the
+// short ones fill the tail.
+constexpr int kMaxMapSeqs = 128;
+struct AttnWorkMap {
+    int32_t n_seq;                      // sequences with rows; 0: plain (b, g, rt) order
+    int32_t per_head;                   // row tiles of all sequences, one kv head
+    int32_t order[kMaxMapSeqs];         // sequence in each slot
+    int32_t cum[kMaxMapSeqs + 1];       // row tiles before each slot
+};
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
     const int32_t *__restrict__ prefix_lens, const int32_t *__restrict__ cu_suffix, int32_t Hq,
-    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, u16 *__restrict__ out)
+    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, u16 *__restrict__ out, const AttnWorkMap wm)
 {
     using Geo = TileGeom<D>;
     constexpr int CPR = Geo::CPR;
@@ -149,16 +163,42 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // the whole array is reused for the merge at the end.
     __shared__ __attribute__((aligned(1024))) char lds[2][2 * (Geo::KBYTES + Geo::VBYTES)];
 
-    // XCD-aware order: workgroup L runs on XCD L % 8, so consecutive work items
-    // (the row tiles of one (sequence, kv head), which read the same K/V) are
-    // given to workgroups of one XCD and share its L2.
-    const int n_work = row_tiles * Hkv * B;
-    const int per_xcd = (int)(gridDim.x / kXcds);
-    const int w = (int)(blockIdx.x % kXcds) * per_xcd + (int)(blockIdx.x / kXcds);
-    if (w >= n_work) return;
-    const int rt = w % row_tiles;
-    const int g = (w / row_tiles) % Hkv;
-    const int b = w / (row_tiles * Hkv);
+    // XCD-aware order: workgroup L runs on XCD L % 8. The row tiles of one (sequence,
+    // kv head), which read the same K/V, go to workgroups of one XCD and share its L2.
+    // With the work map and Hkv a multiple of 8, XCD x takes kv heads x, x+8, ... of
+    // every sequence, so the eight XCDs get equal work.
+    int b, g, rt;
+    {
+        const int x = (int)(blockIdx.x % kXcds), i = (int)(blockIdx.x / kXcds);
+        const int per_xcd = (int)(gridDim.x / kXcds);
+        if (wm.n_seq > 0) {
+            int j;
+            if (Hkv % kXcds == 0) {
+                const int hh = i / wm.per_head;
+                g = x + kXcds * hh;
+                j = i - hh * wm.per_head;
+            } else {
+                const int w = x * per_xcd + i;
+                g = w / wm.per_head;
+                j = w - g * wm.per_head;
+            }
+            if (g >= Hkv) return;
+            int lo = 0, hi = wm.n_seq - 1;               // slot with cum[lo] <= j < cum[lo + 1]
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (wm.cum[mid] <= j) lo = mid; else hi = mid - 1;
+            }
+            b = wm.order[lo];
+            rt = wm.cum[lo + 1] - 1 - j;
+        } else {
+            const int n_work = row_tiles * Hkv * B;
+            const int w = x * per_xcd + i;
+            if (w >= n_work) return;
+            rt = w % row_tiles;
+            g = (w / row_tiles) % Hkv;
+            b = w / (row_tiles * Hkv);
+        }
+    }
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2;              // 0: first half of the keys, 1: second half
@@ -560,12 +600,39 @@ int attn_rows_per_workgroup(int) { return kRowsPerWG; }
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *block_tables, int32_t max_blocks,
                                       const int32_t *prefix_lens, const int32_t *cu_suffix,
+                                      const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s)
 {
-    const int64_t n_work = (int64_t)max_row_tiles * pool.num_kv_heads * B;
-    const dim3 grid((unsigned)(((n_work + kXcds - 1) / kXcds) * kXcds));
+    const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv;
+    AttnWorkMap wm;
+    wm.n_seq = 0;
+    wm.per_head = 0;
+    int64_t n_items;
+    if (B <= kMaxMapSeqs) {
+        int32_t tiles[kMaxMapSeqs], keys[kMaxMapSeqs];
+        int n = 0;
+        for (int b = 0; b < B; ++b) {
+            const int64_t sb = (int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b];
+            if (sb <= 0) continue;
+            wm.order[n] = b;
+            tiles[b] = (int32_t)((sb * G + kRowsPerWG - 1) / kRowsPerWG);
+            keys[b] = (int32_t)(host_prefix_lens[b] + sb);
+            ++n;
+        }
+        std::stable_sort(wm.order, wm.order + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
+        wm.cum[0] = 0;
+        for (int k = 0; k < n; ++k) wm.cum[k + 1] = wm.cum[k] + tiles[wm.order[k]];
+        wm.n_seq = n;
+        wm.per_head = wm.cum[n];
+        if (n == 0) return hipSuccess;
+        n_items = (Hkv % kXcds == 0) ? (int64_t)wm.per_head * Hkv
+                                     : ((int64_t)wm.per_head * Hkv + kXcds - 1) / kXcds * kXcds;
+    } else {
+        n_items = ((int64_t)max_row_tiles * Hkv * B + kXcds - 1) / kXcds * kXcds;
+    }
+    const dim3 grid((unsigned)n_items);
     const float scale_log2 = sm_scale * kLog2e;
     auto *qq = static_cast<const u16 *>(q);
     auto *pk = static_cast<const u16 *>(pool.k);
@@ -574,11 +641,11 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
     if (pool.head_dim == 128)
         hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo, wm);
     else
         hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo, wm);
     return hipGetLastError();
 }
 

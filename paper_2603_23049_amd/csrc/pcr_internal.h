@@ -39,6 +39,7 @@ hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t ho
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *block_tables, int32_t max_blocks,
                                       const int32_t *prefix_lens, const int32_t *cu_suffix,
+                                      const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s);

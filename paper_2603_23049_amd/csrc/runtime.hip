@@ -362,7 +362,8 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const
         return fail(PCR_ERR_INVALID_ARG, "%s: q/out must be 16-byte aligned", who);
     if (max_tiles * pool->num_kv_heads * (int64_t)B > (int64_t)1 << 30)
         return fail(PCR_ERR_UNSUPPORTED, "%s: batch too large for one launch", who);
-    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix, B,
+    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                              host_prefix_lens, host_cu_suffix, B,
                                               num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,
                                               static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "pcr_prefix_prefill_attn: launch");

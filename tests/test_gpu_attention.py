@@ -132,3 +132,31 @@ def test_l70b_shape_sampled_rows():
     want = _oracle(b, data, pk0, pv0, rows=rows)
     got = L.out_f64()[rows[:, 0], rows[:, 1]]
     _check(got, want, "l70b sampled")
+
+
+def test_rag_mix_sampled_rows_and_pool():
+    """RAG-mix batch (16 ragged requests, prefixes hit in a warmed prefix tree, shared
+    tree chunks loaded once, two sequences with no hit): the pool after load + append is
+    the oracle's bit for bit, and sampled rows of every sequence (first, second, middle
+    and last suffix rows plus a spread) match the oracle for every head."""
+    from paper_2603_23049_amd import prefix_tree
+    b = prefix_tree.rag_mix_batch()
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention rag_mix (T={b.T}, {b.note})")
+    L = _run(b, data, pk0, pv0)
+    plan = odm.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, BS)
+    pk, pv = odm.pool_after_layer(pk0, pv0, data.host_k, data.host_v, plan, data.k_new, data.v_new, BS)
+    assert np.array_equal(u16(L.pool.k).reshape(pk.shape), pk), "pool K after load + append"
+    assert np.array_equal(u16(L.pool.v).reshape(pv.shape), pv), "pool V after load + append"
+    cu = b.cu_suffix
+    rng = np.random.Generator(np.random.PCG64(404))
+    toks = []
+    for i, s in enumerate(b.suffix_lens):
+        local = {0, 1, s // 2, s - 2, s - 1} | set(rng.integers(0, s, size=4).tolist())
+        toks += [int(cu[i]) + t for t in sorted(local) if 0 <= t < s]
+    rows = np.array([[t, h] for t in toks for h in range(b.num_q_heads)], np.int32)
+    want = oattn.attention(data.q, pk, pv, b.block_tables, np.asarray(b.prefix_lens, np.int32), plan[3],
+                           b.num_kv_heads, BS, rows=rows)
+    got = L.out_f64()[rows[:, 0], rows[:, 1]]
+    _check(got, want, "rag_mix sampled")
