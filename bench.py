@@ -290,6 +290,100 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
             "exposed_ideal_ms_per_layer": load_ms_iso / n if compute_ms_iso >= load_ms_iso else None}
 
 
+def flow_shop3_makespan(load_ms: float, compute_ms: float, offload_ms: float, n: int) -> float:
+    """Least makespan of n identical layers through three in-order queues (load, then
+    compute, then offload): one layer's three steps plus n-1 times the slowest step."""
+    return load_ms + compute_ms + offload_ms + (n - 1) * max(load_ms, compute_ms, offload_ms)
+
+
+def _host_store(batch, n_blocks):
+    import torch
+    from paper_2603_23049_amd import pcr
+    shape = (max(n_blocks, 1), batch.num_kv_heads, batch.block_size * batch.head_dim)
+    return pcr.HostKV(torch.zeros(shape, dtype=torch.int16, pin_memory=True),
+                      torch.zeros(shape, dtype=torch.int16, pin_memory=True), batch.num_kv_heads, batch.head_dim)
+
+
+def measure_offload(batch, reps=6, chunk=256):
+    """Pool-to-host copy of one layer's computed whole chunks, per method; plus a
+    contiguous 256 MiB device-to-pinned copy as the link reference."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    L, bp, _ = _setup_layer(batch)
+    src, dst = pcr.plan_offload(batch.prefix_lens, batch.suffix_lens, batch.block_tables, batch.block_size, chunk)
+    host = _host_store(batch, len(dst))
+    nbytes = len(src) * batch.block_size * batch.num_kv_heads * batch.head_dim * 2 * 2
+    s = torch.cuda.Stream()
+    ws = torch.empty(pcr.staged_workspace_bytes(len(src), batch.num_kv_heads, batch.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    out = {"bytes_per_layer": nbytes, "blocks": int(len(src))}
+    for method in ("kernel_pull", "dma_per_block", "dma_staged"):
+        times = []
+        for r in range(reps + 2):
+            a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            pcr.offload_kv_layer(L.pool, src, host, dst, method=method, stream=s, workspace=ws)
+            e.record(s)
+            e.synchronize()
+            if r >= 2:
+                times.append(a.elapsed_time(e))
+        ms = _median(times)
+        out["kernel_push" if method == "kernel_pull" else method] = {"ms": ms, "GBps": nbytes / ms / 1e6}
+    big = 256 << 20
+    h = torch.empty(big, dtype=torch.uint8, pin_memory=True)
+    d = torch.ones(big, dtype=torch.uint8, device="cuda")
+    times = []
+    for r in range(8):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            a.record(s)
+            h.copy_(d, non_blocking=True)
+            e.record(s)
+        e.synchronize()
+        if r >= 2:
+            times.append(a.elapsed_time(e))
+    out["contiguous_d2h_GBps"] = big / _median(times) / 1e6
+    return out, src, dst
+
+
+def measure_pipeline_offload(batch, method, load_ms_iso, compute_ms_iso, offload_ms_iso, src, dst, reps=2,
+                             distinct=4, offload_method="dma_staged"):
+    """The three-stream pipeline (load, compute, offload of the computed chunks).
+    Exposure per layer = (pipeline time - n x isolated compute) / n; its least value
+    follows from the isolated per-layer times of the three steps."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    n = batch.num_layers
+    layers, bp = _setup_pipeline(batch, distinct)
+    outs = [_host_store(batch, len(dst)) for _ in range(min(distinct, n))]
+    dsts = [outs[l % len(outs)] for l in range(n)]
+    cs, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    ws = torch.empty(pcr.staged_workspace_bytes(len(src), batch.num_kv_heads, batch.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    runs = []
+    for r in range(reps + 1):
+        t = pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
+                                     offload_method=offload_method, workspace=ws, timing=True)
+        if r >= 1:
+            runs.append(t)
+    best = min(runs, key=lambda t: t["total_ms"])
+    e_raw = best["total_ms"] / n - compute_ms_iso
+    bound = flow_shop3_makespan(load_ms_iso, compute_ms_iso, offload_ms_iso, n)
+    e_min = bound / n - compute_ms_iso
+    del layers, outs, dsts
+    torch.cuda.synchronize()
+    return {"layers": n, "workload": batch.name, "method": method, "offload_method": offload_method,
+            "distinct_layer_data": distinct, "total_ms": best["total_ms"], "compute_end_ms": best["compute_end_ms"],
+            "load_ms_per_layer_isolated": load_ms_iso, "compute_ms_per_layer_isolated": compute_ms_iso,
+            "offload_ms_per_layer_isolated": offload_ms_iso,
+            "offload_ms_per_layer_in_pipeline": float(np.median(best["offload_ms"])),
+            "exposed_ms_per_layer": e_raw, "exposed_min_ms_per_layer": e_min,
+            "exposed_over_min_ms_per_layer": e_raw - e_min,
+            "exposed_frac_of_transfer": e_raw / (load_ms_iso + offload_ms_iso),
+            "bound_makespan_ms": bound,
+            "synchronous_ms": n * (load_ms_iso + compute_ms_iso + offload_ms_iso)}
+
+
 def cpu_baseline(batch, budget_s=12.0):
     """The fp64 oracle (as it stands) on the same layer, repeated until about budget_s
     of CPU time has passed; TFLOP/s by the layer's causal-exact FLOPs."""
@@ -380,6 +474,10 @@ def main(argv=None):
                             "T": rb.T, "hit_ratio": rb.extra["hit_ratio"],
                             "load_bytes": load_bytes(rb.prefix_lens, rb.num_kv_heads, rb.head_dim)}
         if not args.no_pipeline:
+            ob = synth.l8b_pipe32(suffix=6144)
+            _say(f"[bench] offload: {ob.name}")
+            off, osrc, odst = measure_offload(ob)
+            extra["offload"] = off
             for pb in (synth.l70b_pipe80(), synth.l8b_pipe32(suffix=6144)):
                 _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, 4 distinct layer data sets)")
                 pst = measure_step(pb, 10, 3)
@@ -389,6 +487,12 @@ def main(argv=None):
                 pipelines[pb.name]["attn_tflops"] = attention_flops(
                     pb.prefix_lens, pb.suffix_lens, pb.num_q_heads, pb.head_dim) / (pst["attn_ms"] * 1e-3) / 1e12
                 pipelines[pb.name]["load_GBps"] = pld[method]["GBps"]
+                if pb.name == ob.name:
+                    _say(f"[bench] pipeline with offload: {pb.name}")
+                    for om, key in (("dma_staged", "dma_staged"), ("kernel_pull", "kernel_push")):
+                        pipelines[f"{pb.name}_offload_{key}"] = measure_pipeline_offload(
+                            pb, method, pld[method]["ms"], pst["step_ms"], off[key]["ms"], osrc, odst,
+                            offload_method=om)
     cpu = None
     if not args.no_cpu_baseline:
         _say("[bench] cpu baseline (oracle)")
@@ -422,6 +526,7 @@ def main(argv=None):
         "pipeline": pipe,
         "pipelines": pipelines or None,
         "rag_mix": extra.get("rag_mix"),
+        "offload": extra.get("offload"),
         "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
         "cpu_baseline": cpu,
         "wall_s_timed": st["wall_s"],

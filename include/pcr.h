@@ -84,8 +84,12 @@ typedef enum pcr_load_method {
                                    blocks merged into one copy */
     PCR_LOAD_DMA_PER_BLOCK = 2, /* one hipMemcpyAsync per block and per K/V (the
                                    block-by-block baseline of Sec. 5) */
-    PCR_LOAD_KERNEL_PULL = 3    /* a copy kernel on the given stream reads the pinned host
+    PCR_LOAD_KERNEL_PULL = 3,   /* a copy kernel on the given stream reads the pinned host
                                    pages directly and writes the pool blocks */
+    PCR_LOAD_DMA_STAGED = 4     /* through a device workspace: the copy engines move whole
+                                   runs of consecutive host blocks over the host link and a
+                                   kernel scatters (load) or gathers (offload) the pool blocks
+                                   at HBM speed; only with the *_staged entry points */
 } pcr_load_method;
 
 /*
@@ -136,6 +140,69 @@ pcr_status pcr_load_kv_layer(const pcr_host_kv *src, const int32_t *src_blocks,
 pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_blocks,
                                     const pcr_kv_pool *dst, const int32_t *dst_blocks, int32_t n,
                                     pcr_load_method method, void *copy_stream);
+
+/*
+ * pcr_plan_offload -- the GPU-to-host list of one batch (Alg. 1: a chunk of a
+ * scheduled request that no cache tier holds is computed, then goes on the
+ * GPU-to-CPU list, "LayerwiseDownload"). For each sequence b, every whole chunk of
+ * chunk_tokens tokens (aligned to multiples of chunk_tokens from the sequence
+ * start) that lies entirely inside the computed range [prefix_lens[b],
+ * prefix_lens[b] + suffix_lens[b]) is listed block by block, sequences in order:
+ * src_blocks[i] is its pool block (from block_tables) and dst_blocks[i] =
+ * first_dst_block + i (host-store blocks in consecutive order, ready to become the
+ * chunks' cache entries). A trailing partial chunk is not offloaded.
+ *   chunk_tokens   a positive multiple of block_size
+ *   cap            capacity of src_blocks / dst_blocks; *n_pairs receives the count
+ * Errors: PCR_ERR_INVALID_ARG for negative lengths, a chunk size that is not a
+ * multiple of the block size, a missing pool block (-1 or past max_blocks), or
+ * more pairs than cap (nothing useful is written then).
+ */
+pcr_status pcr_plan_offload(int32_t B, const int32_t *prefix_lens, const int32_t *suffix_lens,
+                            const int32_t *block_tables, int32_t max_blocks, int32_t block_size,
+                            int32_t chunk_tokens, int32_t first_dst_block,
+                            int32_t *src_blocks, int32_t *dst_blocks, int32_t cap, int32_t *n_pairs);
+
+/*
+ * pcr_offload_kv_layer -- enqueue the pool-to-host copy of one layer's new blocks
+ * (Alg. 1 "LayerwiseDownload"; Sec. 4.3: offloading a layer starts as soon as
+ * that layer's computation ends; Sec. 5: on a stream of its own). For each i < n:
+ * host block dst_blocks[i] of dst becomes a bitwise copy of pool block
+ * src_blocks[i] of src (K and V, all kv heads). Host arrays, range-checked on the
+ * host; dst ids must be distinct; dst must be pinned (PCR_ERR_NOT_PINNED
+ * otherwise). The caller orders the call after the compute that wrote the
+ * blocks (an event from the compute stream).
+ * Methods: PCR_LOAD_AUTO and PCR_LOAD_KERNEL_PULL select the copy kernel, which
+ * here reads the pool and writes the pinned host pages directly;
+ * PCR_LOAD_DMA_PER_BLOCK issues one hipMemcpyAsync per block and per K/V;
+ * PCR_LOAD_DMA_BATCH one batched copy (PCR_ERR_UNSUPPORTED without it).
+ */
+pcr_status pcr_offload_kv_layer(const pcr_kv_pool *src, const int32_t *src_blocks,
+                                const pcr_host_kv *dst, const int32_t *dst_blocks, int32_t n,
+                                void *stream);
+pcr_status pcr_offload_kv_layer_method(const pcr_kv_pool *src, const int32_t *src_blocks,
+                                       const pcr_host_kv *dst, const int32_t *dst_blocks, int32_t n,
+                                       pcr_load_method method, void *stream);
+
+/*
+ * The staged forms of the two copies (PCR_LOAD_DMA_STAGED). workspace: device
+ * memory owned by the caller, 16-byte aligned, at least 2 * n * block bytes
+ * (block bytes = block_size * num_kv_heads * head_dim * 2); its contents are
+ * scratch. Work on one stream is ordered, so one workspace serves every call on
+ * that stream; calls on different streams that may overlap need their own.
+ * Offload: a kernel gathers the listed pool blocks into the workspace, then one
+ * copy-engine transfer per run of consecutive dst host blocks. Load: one transfer
+ * per run of consecutive src host blocks into the workspace, then a kernel
+ * scatters the blocks into the pool. The long host-link transfers then occupy no
+ * compute unit (a kernel that writes host memory directly slows kernels running
+ * beside it far more than the copy engines do). PCR_ERR_INVALID_ARG if the
+ * workspace is missing or too small.
+ */
+pcr_status pcr_offload_kv_layer_staged(const pcr_kv_pool *src, const int32_t *src_blocks,
+                                       const pcr_host_kv *dst, const int32_t *dst_blocks, int32_t n,
+                                       void *workspace, int64_t workspace_bytes, void *stream);
+pcr_status pcr_load_kv_layer_staged(const pcr_host_kv *src, const int32_t *src_blocks,
+                                    const pcr_kv_pool *dst, const int32_t *dst_blocks, int32_t n,
+                                    void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * pcr_append_kv -- write the new tokens' K/V into the pool (the KV write that
@@ -226,6 +293,32 @@ typedef struct pcr_batch {
 pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
                             pcr_load_method method, void *copy_stream, void *compute_stream,
                             float *timing_ms);
+
+/*
+ * pcr_pipeline_run_offload -- the three-stream form (Sec. 5: upload, compute and
+ * download streams; Sec. 4.3: offloading a layer starts when its computation
+ * ends). As pcr_pipeline_run, and in addition, after layer l's compute,
+ * offload_stream waits for it and copies pool blocks off_src[i] of layer l into
+ * host blocks off_dst[i] of offload_dst[l] (i < n_off, host arrays, the same list
+ * for every layer) with offload_method. offload_dst: host array of n_layers pinned
+ * stores. workspace / workspace_bytes: the staging memory of the offload stream
+ * when offload_method is PCR_LOAD_DMA_STAGED (else unused, may be NULL / 0).
+ * Before its first load the copy stream also waits for the work already queued on
+ * offload_stream, so a load never overwrites a pool an earlier offload is still
+ * reading. The three streams must differ.
+ * timing_ms: NULL, or host float[6*n_layers + 3]; when given the call waits for
+ * the last offload and fills, per layer l: [6l] load ms, [6l+1] compute ms,
+ * [6l+2] compute-stream wait before the layer, [6l+3] end of the layer's compute
+ * and [6l+5] end of its offload (both relative to the pipeline start), [6l+4]
+ * offload ms; then [6n] the whole pipeline ms (to the last offload end), [6n+1]
+ * the sum of compute ms, [6n+2] the end of the last compute.
+ */
+pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_kv *offload_dst,
+                                    int32_t n_layers, const pcr_batch *batch, const int32_t *off_src,
+                                    const int32_t *off_dst, int32_t n_off, pcr_load_method method,
+                                    pcr_load_method offload_method, void *workspace, int64_t workspace_bytes,
+                                    void *copy_stream, void *compute_stream, void *offload_stream,
+                                    float *timing_ms);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *pcr_last_error(void);

@@ -13,6 +13,10 @@ Steps (the layer step of Sec. 4.3 / Alg. 1, on a paged pool as in Sec. 5):
              other pool block keeps its bits.
   append  -- the new tokens' K/V rows go to their slots, bit for bit.
   gather  -- read a sequence's K/V back in logical token order, bit for bit.
+  plan_offload -- the "gpu_to_cpu" list of Alg. 1: every whole chunk of a
+             sequence's computed tokens (chunks aligned to the sequence start)
+             goes to the host store after compute, block by block.
+  offload -- host[dst] <- pool[src] for every listed pair, bit for bit.
 
 Pool / host-store block layout (bf16 bit patterns, one layer; per block and
 kv head a payload of block_size*head_dim elements):
@@ -138,3 +142,34 @@ def pool_after_layer(pool_k, pool_v, host_k, host_v, batch_plan, k_new, v_new, b
     load(pk, pv, host_k, host_v, src, dst)
     append(pk, pv, k_new, v_new, slots, block_size)
     return pk, pv
+
+
+def plan_offload(prefix_lens: Sequence[int], suffix_lens: Sequence[int], block_tables: np.ndarray,
+                 block_size: int = 16, chunk_tokens: int = 256, first_dst_block: int = 0):
+    """(src pool blocks, dst host blocks): for every sequence, the blocks of each whole
+    chunk [c*chunk, (c+1)*chunk) that lies inside its computed range [p, p+s), chunks
+    and blocks in order; host blocks numbered from first_dst_block."""
+    if chunk_tokens % block_size:
+        raise PlanError("chunk size must be a multiple of the block size")
+    src, dst = [], []
+    for b, (p, s) in enumerate(zip(prefix_lens, suffix_lens)):
+        p, s = int(p), int(s)
+        c = 0
+        while (c + 1) * chunk_tokens <= p + s:
+            if c * chunk_tokens >= p:                          # the chunk is all computed tokens
+                for t in range(c * chunk_tokens, (c + 1) * chunk_tokens, block_size):
+                    blk = int(block_tables[b][t // block_size])
+                    if blk < 0:
+                        raise PlanError(f"sequence {b} token {t} has no pool block")
+                    src.append(blk)
+                    dst.append(first_dst_block + len(dst))
+            c += 1
+    return np.asarray(src, np.int32), np.asarray(dst, np.int32)
+
+
+def offload(pool_k: np.ndarray, pool_v: np.ndarray, host_k: np.ndarray, host_v: np.ndarray,
+            src_blocks: Sequence[int], dst_blocks: Sequence[int]) -> None:
+    """In place: host[dst_i] <- pool[src_i] for every pair (whole block, all kv heads)."""
+    for s_blk, d_blk in zip(src_blocks, dst_blocks):
+        host_k[int(d_blk)] = pool_k[int(s_blk)]
+        host_v[int(d_blk)] = pool_v[int(s_blk)]

@@ -113,13 +113,18 @@ __device__ __forceinline__ void phase_barrier()
 // completion of these loads on vmcnt only; the kernel waits for them explicitly
 // before the barrier that precedes their first reader.
 // The source is a wave-uniform base (SGPR pair) plus a 32-bit per-lane byte offset.
-// lds_dst is an LDS byte address (M0 form).
+// lds_dst is an LDS byte address (M0 form). M0 is a register the compiler reserves:
+// it does not honour the clobber, and relies on M0 only for instructions that read
+// it, of which this file has none besides these loads (each sets it first).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const char *base, uint32_t lane_off, uint32_t lds_dst)
 {
     const unsigned m0 = __builtin_amdgcn_readfirstlane(lds_dst);
     asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(base), "s"(m0)
                  : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 // Wait until at most N vector-memory operations of this wave are outstanding
 // (the N most recent may still be in flight).
@@ -367,7 +372,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
         constexpr int NPV = DO_PV ? kTileBlocks * MT : 0, NQK = DO_QK ? 2 * KSTEPS : 0, NALL = NPV + NQK;
         constexpr int NLD = DO_QK ? kVLoads + kKLoads : 0;
-        constexpr int EVERY = NLD ? (NALL / NLD > 0 ? NALL / NLD : 1) : 1;
+        constexpr int NLD1 = NLD > 0 ? NLD : 1;
+        constexpr int EVERY = NALL / NLD1 > 0 ? NALL / NLD1 : 1;
         constexpr int kAhead = KAHEAD;
         const char *tv = vbuf(j);
         const char *tk = kbuf(j + 1);

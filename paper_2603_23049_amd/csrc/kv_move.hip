@@ -143,9 +143,11 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// host pull: each workgroup copies whole blocks (K or V of one pair) from the
-// pinned host store into the pool, 16 B per lane, 8 loads in flight per lane
-// before their stores. Grid-stride over the 2*n block copies.
+// host pull / push: each workgroup copies whole blocks (K or V of one pair)
+// between the pinned host store and the pool, 16 B per lane, 8 loads in flight
+// per lane before their stores. Grid-stride over the 2*n block copies. Pull
+// (host -> pool) reads the host pages with non-temporal loads; push (pool ->
+// host) writes them with non-temporal stores, so host data never occupies L2.
 // ---------------------------------------------------------------------------
 constexpr int kPullUnroll = 8;
 // Workgroups of one pull launch: 32 x 256 lanes x 8 x 16 B = 1 MiB in flight, enough
@@ -153,9 +155,12 @@ constexpr int kPullUnroll = 8;
 // (on MI355X, 16 workgroups reach about 85% of the link, 32 and more the full link).
 constexpr int kPullWorkgroups = 32;
 
-__global__ __launch_bounds__(256) void pull_blocks_kernel(
-    const u32x4 *__restrict__ host_k, const u32x4 *__restrict__ host_v, int64_t host_blocks,
-    u32x4 *__restrict__ pool_k, u32x4 *__restrict__ pool_v, int32_t pool_blocks,
+enum CopyDir { kHostToDevice = 0, kDeviceToHost = 1, kDeviceToDevice = 2 };
+
+template <int kDir>
+__global__ __launch_bounds__(256) void copy_blocks_kernel(
+    const u32x4 *__restrict__ src_k, const u32x4 *__restrict__ src_v, int64_t src_blocks,
+    u32x4 *__restrict__ dst_k, u32x4 *__restrict__ dst_v, int64_t dst_blocks,
     int64_t block_vecs, const PullArgs args)
 {
     const int units = 2 * args.n;
@@ -163,20 +168,23 @@ __global__ __launch_bounds__(256) void pull_blocks_kernel(
         const int pair = u >> 1;
         const bool is_v = u & 1;
         const int64_t sb = args.src[pair], db = args.dst[pair];
-        if (sb < 0 || sb >= host_blocks || db < 0 || db >= pool_blocks) continue;
-        const u32x4 *src = (is_v ? host_v : host_k) + sb * block_vecs;
-        u32x4 *dst = (is_v ? pool_v : pool_k) + db * block_vecs;
+        if (sb < 0 || sb >= src_blocks || db < 0 || db >= dst_blocks) continue;
+        const u32x4 *src = (is_v ? src_v : src_k) + sb * block_vecs;
+        u32x4 *dst = (is_v ? dst_v : dst_k) + db * block_vecs;
         for (int64_t base = 0; base < block_vecs; base += 256 * kPullUnroll) {
             u32x4 r[kPullUnroll];
 #pragma unroll
             for (int k = 0; k < kPullUnroll; ++k) {
                 const int64_t i = base + k * 256 + threadIdx.x;
-                if (i < block_vecs) r[k] = __builtin_nontemporal_load(src + i);
+                if (i < block_vecs) r[k] = kDir == kHostToDevice ? __builtin_nontemporal_load(src + i) : src[i];
             }
 #pragma unroll
             for (int k = 0; k < kPullUnroll; ++k) {
                 const int64_t i = base + k * 256 + threadIdx.x;
-                if (i < block_vecs) dst[i] = r[k];
+                if (i < block_vecs) {
+                    if (kDir == kDeviceToHost) __builtin_nontemporal_store(r[k], dst + i);
+                    else dst[i] = r[k];
+                }
             }
         }
     }
@@ -226,10 +234,36 @@ hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t ho
     if (args.n <= 0) return hipSuccess;
     const int units = 2 * args.n;
     const int grid = units < kPullWorkgroups ? units : kPullWorkgroups;
-    hipLaunchKernelGGL(pull_blocks_kernel, dim3(grid), dim3(256), 0, s,
+    hipLaunchKernelGGL(copy_blocks_kernel<kHostToDevice>, dim3(grid), dim3(256), 0, s,
                        static_cast<const u32x4 *>(host_k), static_cast<const u32x4 *>(host_v),
                        host_blocks, static_cast<u32x4 *>(pool_k), static_cast<u32x4 *>(pool_v),
-                       pool_blocks, block_bytes / 16, args);
+                       (int64_t)pool_blocks, block_bytes / 16, args);
+    return hipGetLastError();
+}
+
+hipError_t launch_push_blocks(const void *pool_k, const void *pool_v, int32_t pool_blocks, void *host_k,
+                              void *host_v, int64_t host_blocks, int64_t block_bytes, const PullArgs &args,
+                              hipStream_t s)
+{
+    if (args.n <= 0) return hipSuccess;
+    const int units = 2 * args.n;
+    const int grid = units < kPullWorkgroups ? units : kPullWorkgroups;
+    hipLaunchKernelGGL(copy_blocks_kernel<kDeviceToHost>, dim3(grid), dim3(256), 0, s,
+                       static_cast<const u32x4 *>(pool_k), static_cast<const u32x4 *>(pool_v),
+                       (int64_t)pool_blocks, static_cast<u32x4 *>(host_k), static_cast<u32x4 *>(host_v),
+                       host_blocks, block_bytes / 16, args);
+    return hipGetLastError();
+}
+
+hipError_t launch_device_blocks(const void *src_k, const void *src_v, int64_t src_blocks, void *dst_k, void *dst_v,
+                                int64_t dst_blocks, int64_t block_bytes, const PullArgs &args, hipStream_t s)
+{
+    if (args.n <= 0) return hipSuccess;
+    // HBM to HBM: one workgroup per block copy, all CUs if there is work for them
+    const int grid = 2 * args.n;
+    hipLaunchKernelGGL(copy_blocks_kernel<kDeviceToDevice>, dim3(grid), dim3(256), 0, s,
+                       static_cast<const u32x4 *>(src_k), static_cast<const u32x4 *>(src_v), src_blocks,
+                       static_cast<u32x4 *>(dst_k), static_cast<u32x4 *>(dst_v), dst_blocks, block_bytes / 16, args);
     return hipGetLastError();
 }
 

@@ -34,6 +34,11 @@ hipError_t launch_gather_kv(const pcr_kv_pool &pool, const int32_t *block_tables
 hipError_t launch_pull_blocks(const void *host_k, const void *host_v, int64_t host_blocks,
                               void *pool_k, void *pool_v, int32_t pool_blocks, int64_t block_bytes,
                               const PullArgs &args, hipStream_t s);
+hipError_t launch_device_blocks(const void *src_k, const void *src_v, int64_t src_blocks, void *dst_k, void *dst_v,
+                                int64_t dst_blocks, int64_t block_bytes, const PullArgs &args, hipStream_t s);
+hipError_t launch_push_blocks(const void *pool_k, const void *pool_v, int32_t pool_blocks, void *host_k,
+                              void *host_v, int64_t host_blocks, int64_t block_bytes, const PullArgs &args,
+                              hipStream_t s);
 
 // Attention launcher (attn.hip).
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
@@ -43,6 +48,12 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s);
+
+// Pool-to-host offload with any method (the staged one takes the workspace); used by
+// the pipeline, which chooses the method per call.
+pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                        const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *workspace,
+                        int64_t workspace_bytes, void *stream);
 
 // Rows of packed (token, head-in-group) queries one attention workgroup handles.
 int attn_rows_per_workgroup(int head_dim);

@@ -1,11 +1,13 @@
-// Two-stream layer pipeline (Sec. 4.3 layer-wise overlap; Alg. 1 LayerwiseUpload
-// then WaitForUploadEvents before each layer's compute).
+// Layer pipeline (Sec. 4.3 layer-wise overlap; Alg. 1 LayerwiseUpload, then
+// WaitForUploadEvents before each layer's compute, and LayerwiseDownload).
 //
 // Every layer has its own pool, so all loads are enqueued up front on the copy
 // stream, each followed by an event; the compute stream waits for layer l's
-// event and then runs layer l's append and attention. The copy stream first
-// waits for everything already queued on the compute stream, so a load never
-// overwrites a pool that earlier compute is still reading.
+// event and then runs layer l's append and attention. With an offload stream
+// (the three-stream form of Sec. 5), that stream waits for layer l's compute and
+// then copies the layer's new blocks to the host store. The copy stream first
+// waits for everything already queued on the compute (and offload) stream, so a
+// load never overwrites a pool that earlier work is still reading.
 #include <vector>
 
 #include "pcr_internal.h"
@@ -48,30 +50,43 @@ float elapsed(hipEvent_t a, hipEvent_t b)
 
 using namespace pcr;
 
-extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
-                                       pcr_load_method method, void *copy_stream, void *compute_stream,
-                                       float *timing_ms)
+namespace {
+
+pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_dst, int32_t n_layers,
+                        const pcr_batch *batch, const int32_t *off_src, const int32_t *off_dst, int32_t n_off,
+                        pcr_load_method method, pcr_load_method offload_method, void *workspace,
+                        int64_t workspace_bytes, void *copy_stream, void *compute_stream, void *offload_stream,
+                        bool with_offload, float *timing_ms, const char *who)
 {
-    const char *who = "pcr_pipeline_run";
     if (n_layers < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_layers < 0", who);
     if (n_layers == 0) return PCR_OK;
     if (!layers || !batch) return fail(PCR_ERR_INVALID_ARG, "%s: NULL layers or batch", who);
     if (copy_stream == compute_stream)
         return fail(PCR_ERR_INVALID_ARG, "%s: copy and compute streams must differ", who);
+    if (with_offload) {
+        if (offload_stream == compute_stream || offload_stream == copy_stream)
+            return fail(PCR_ERR_INVALID_ARG, "%s: the offload stream must differ from the other two", who);
+        if (n_off < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_off < 0", who);
+        if (n_off > 0 && (!offload_dst || !off_src || !off_dst))
+            return fail(PCR_ERR_INVALID_ARG, "%s: NULL offload argument", who);
+    }
     hipStream_t cs = static_cast<hipStream_t>(copy_stream);
     hipStream_t ks = static_cast<hipStream_t>(compute_stream);
+    hipStream_t os = static_cast<hipStream_t>(offload_stream);
     const bool timed = timing_ms != nullptr;
     const size_t n = (size_t)n_layers;
 
-    // timed: [0] start, [1+l] load start, [1+n+l] loaded, [1+2n+l] compute start, [1+3n+l] compute end
+    // events: [0] start, [1] offload-stream start, then per layer: load start, loaded,
+    // compute start, compute end, offload start, offload end (timed); loaded and
+    // compute end only (untimed)
     EventPool &pool = timed ? g_timed_events : g_sync_events;
-    hipError_t e = pool.ensure(timed ? 1 + 4 * n : 1 + n);
+    const size_t per = timed ? 6 : 2;
+    hipError_t e = pool.ensure(2 + per * n);
     if (e != hipSuccess) return hip_fail(e, "pcr_pipeline_run: hipEventCreate");
-    hipEvent_t ev_start = pool.ev[0];
-    auto ev_lstart = [&](size_t l) { return pool.ev[1 + l]; };
-    auto ev_loaded = [&](size_t l) { return timed ? pool.ev[1 + n + l] : pool.ev[1 + l]; };
-    auto ev_cstart = [&](size_t l) { return pool.ev[1 + 2 * n + l]; };
-    auto ev_cend = [&](size_t l) { return pool.ev[1 + 3 * n + l]; };
+    hipEvent_t ev_start = pool.ev[0], ev_ostart = pool.ev[1];
+    auto ev = [&](size_t l, int k) { return pool.ev[2 + per * l + k]; };
+    auto ev_loaded = [&](size_t l) { return ev(l, timed ? 1 : 0); };
+    auto ev_cend = [&](size_t l) { return ev(l, timed ? 3 : 1); };
 
 #define PCR_HIP(call, what)                          \
     do {                                             \
@@ -81,8 +96,12 @@ extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_lay
 
     PCR_HIP(hipEventRecord(ev_start, ks), "pcr_pipeline_run: record start");
     PCR_HIP(hipStreamWaitEvent(cs, ev_start, 0), "pcr_pipeline_run: copy waits for compute");
+    if (with_offload) {
+        PCR_HIP(hipEventRecord(ev_ostart, os), "pcr_pipeline_run: record offload start");
+        PCR_HIP(hipStreamWaitEvent(cs, ev_ostart, 0), "pcr_pipeline_run: copy waits for offload");
+    }
     for (size_t l = 0; l < n; ++l) {
-        if (timed) PCR_HIP(hipEventRecord(ev_lstart(l), cs), "pcr_pipeline_run: record load start");
+        if (timed) PCR_HIP(hipEventRecord(ev(l, 0), cs), "pcr_pipeline_run: record load start");
         pcr_status st = pcr_load_kv_layer_method(&layers[l].host, batch->src_blocks, &layers[l].pool,
                                                  batch->dst_blocks, batch->n_pairs, method, copy_stream);
         if (st) return st;
@@ -90,7 +109,7 @@ extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_lay
     }
     for (size_t l = 0; l < n; ++l) {
         PCR_HIP(hipStreamWaitEvent(ks, ev_loaded(l), 0), "pcr_pipeline_run: compute waits for load");
-        if (timed) PCR_HIP(hipEventRecord(ev_cstart(l), ks), "pcr_pipeline_run: record compute start");
+        if (timed) PCR_HIP(hipEventRecord(ev(l, 2), ks), "pcr_pipeline_run: record compute start");
         pcr_status st = pcr_append_kv(&layers[l].pool, layers[l].k_new, layers[l].v_new, batch->slot_mapping,
                                       batch->T, compute_stream);
         if (st) return st;
@@ -99,24 +118,59 @@ extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_lay
                                      batch->host_cu_suffix, batch->B, batch->num_q_heads, batch->sm_scale,
                                      layers[l].out, compute_stream);
         if (st) return st;
-        if (timed) PCR_HIP(hipEventRecord(ev_cend(l), ks), "pcr_pipeline_run: record compute end");
+        PCR_HIP(hipEventRecord(ev_cend(l), ks), "pcr_pipeline_run: record compute end");
+        if (with_offload) {
+            PCR_HIP(hipStreamWaitEvent(os, ev_cend(l), 0), "pcr_pipeline_run: offload waits for compute");
+            if (timed) PCR_HIP(hipEventRecord(ev(l, 4), os), "pcr_pipeline_run: record offload start");
+            st = offload_with(&layers[l].pool, off_src, &offload_dst[l], off_dst, n_off, offload_method, workspace,
+                              workspace_bytes, offload_stream);
+            if (st) return st;
+            if (timed) PCR_HIP(hipEventRecord(ev(l, 5), os), "pcr_pipeline_run: record offload end");
+        }
     }
     if (!timed) return PCR_OK;
 
-    PCR_HIP(hipEventSynchronize(ev_cend(n - 1)), "pcr_pipeline_run: synchronize");
+    hipEvent_t last = with_offload ? ev(n - 1, 5) : ev_cend(n - 1);
+    PCR_HIP(hipEventSynchronize(last), "pcr_pipeline_run: synchronize");
     double sum_compute = 0.0;
+    const size_t stride = with_offload ? 6 : 4;
     for (size_t l = 0; l < n; ++l) {
-        const float load = elapsed(ev_lstart(l), ev_loaded(l));
-        const float comp = elapsed(ev_cstart(l), ev_cend(l));
-        const float wait = elapsed(l == 0 ? ev_start : ev_cend(l - 1), ev_cstart(l));
-        timing_ms[4 * l + 0] = load;
-        timing_ms[4 * l + 1] = comp;
-        timing_ms[4 * l + 2] = wait;
-        timing_ms[4 * l + 3] = elapsed(ev_start, ev_cend(l));
+        const float comp = elapsed(ev(l, 2), ev_cend(l));
+        timing_ms[stride * l + 0] = elapsed(ev(l, 0), ev_loaded(l));
+        timing_ms[stride * l + 1] = comp;
+        timing_ms[stride * l + 2] = elapsed(l == 0 ? ev_start : ev_cend(l - 1), ev(l, 2));
+        timing_ms[stride * l + 3] = elapsed(ev_start, ev_cend(l));
+        if (with_offload) {
+            timing_ms[stride * l + 4] = elapsed(ev(l, 4), ev(l, 5));
+            timing_ms[stride * l + 5] = elapsed(ev_start, ev(l, 5));
+        }
         sum_compute += comp;
     }
-    timing_ms[4 * n] = elapsed(ev_start, ev_cend(n - 1));
-    timing_ms[4 * n + 1] = (float)sum_compute;
+    timing_ms[stride * n] = elapsed(ev_start, last);
+    timing_ms[stride * n + 1] = (float)sum_compute;
+    if (with_offload) timing_ms[stride * n + 2] = elapsed(ev_start, ev_cend(n - 1));
 #undef PCR_HIP
     return PCR_OK;
+}
+
+}  // namespace
+
+extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
+                                       pcr_load_method method, void *copy_stream, void *compute_stream,
+                                       float *timing_ms)
+{
+    return run_pipeline(layers, nullptr, n_layers, batch, nullptr, nullptr, 0, method, PCR_LOAD_AUTO, nullptr, 0,
+                        copy_stream, compute_stream, nullptr, false, timing_ms, "pcr_pipeline_run");
+}
+
+extern "C" pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_kv *offload_dst,
+                                               int32_t n_layers, const pcr_batch *batch, const int32_t *off_src,
+                                               const int32_t *off_dst, int32_t n_off, pcr_load_method method,
+                                               pcr_load_method offload_method, void *workspace,
+                                               int64_t workspace_bytes, void *copy_stream, void *compute_stream,
+                                               void *offload_stream, float *timing_ms)
+{
+    return run_pipeline(layers, offload_dst, n_layers, batch, off_src, off_dst, n_off, method, offload_method,
+                        workspace, workspace_bytes, copy_stream, compute_stream, offload_stream, true, timing_ms,
+                        "pcr_pipeline_run_offload");
 }

@@ -200,9 +200,65 @@ pcr_status pcr_plan(int32_t B, const int32_t *prefix_lens, const int32_t *suffix
     return PCR_OK;
 }
 
-pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_blocks,
-                                    const pcr_kv_pool *dst, const int32_t *dst_blocks, int32_t n,
-                                    pcr_load_method method, void *copy_stream)
+}  // extern "C"
+
+namespace {
+
+// Workspace check of the staged copies: 2 * n blocks (K then V), 16-byte aligned.
+pcr_status check_workspace(void *ws, int64_t ws_bytes, int32_t n, int64_t bb, const char *who)
+{
+    if (!ws) return fail(PCR_ERR_INVALID_ARG, "%s: the staged method needs a workspace", who);
+    if ((uintptr_t)ws & 15) return fail(PCR_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+    if (ws_bytes < 2 * (int64_t)n * bb)
+        return fail(PCR_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed", who, (long long)ws_bytes,
+                    (long long)(2 * (int64_t)n * bb));
+    return PCR_OK;
+}
+
+// Copy-engine transfers of the runs of consecutive host blocks between the host
+// store and workspace slots 0..n-1 (K region then V region of the workspace).
+pcr_status staged_dma(char *hk, char *hv, char *ws, const int32_t *host_blocks, int32_t n, int64_t bb,
+                      bool to_host, hipStream_t s, const char *who)
+{
+    char *wk = ws, *wv = ws + (int64_t)n * bb;
+    int32_t i = 0;
+    while (i < n) {
+        int32_t j = i + 1;
+        while (j < n && host_blocks[j] == host_blocks[j - 1] + 1) ++j;
+        const int64_t bytes = (int64_t)(j - i) * bb, h = (int64_t)host_blocks[i] * bb, w = (int64_t)i * bb;
+        const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+        hipError_t e = to_host ? hipMemcpyAsync(hk + h, wk + w, bytes, kind, s) : hipMemcpyAsync(wk + w, hk + h, bytes, kind, s);
+        if (e == hipSuccess)
+            e = to_host ? hipMemcpyAsync(hv + h, wv + w, bytes, kind, s) : hipMemcpyAsync(wv + w, hv + h, bytes, kind, s);
+        if (e != hipSuccess) return hip_fail(e, who);
+        i = j;
+    }
+    return PCR_OK;
+}
+
+// Kernel copies between listed pool blocks and workspace slots, in slices.
+pcr_status staged_kernel(const pcr_kv_pool *pool, char *ws, const int32_t *pool_blocks, int32_t n, int64_t bb,
+                         bool pool_to_ws, hipStream_t s, const char *who)
+{
+    char *wk = ws, *wv = ws + (int64_t)n * bb;
+    for (int32_t off = 0; off < n; off += kPullPairsPerLaunch) {
+        PullArgs a;
+        a.n = std::min<int32_t>(kPullPairsPerLaunch, n - off);
+        for (int32_t k = 0; k < a.n; ++k) {
+            a.src[k] = pool_to_ws ? pool_blocks[off + k] : off + k;
+            a.dst[k] = pool_to_ws ? off + k : pool_blocks[off + k];
+        }
+        hipError_t e = pool_to_ws
+            ? launch_device_blocks(pool->k, pool->v, pool->num_blocks, wk, wv, n, bb, a, s)
+            : launch_device_blocks(wk, wv, n, pool->k, pool->v, pool->num_blocks, bb, a, s);
+        if (e != hipSuccess) return hip_fail(e, who);
+    }
+    return PCR_OK;
+}
+
+pcr_status load_impl(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
+                     const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *ws, int64_t ws_bytes,
+                     void *copy_stream)
 {
     g_err[0] = 0;
     const char *who = "pcr_load_kv_layer";
@@ -216,7 +272,7 @@ pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_b
     if (src->block_size != dst->block_size || src->num_kv_heads != dst->num_kv_heads ||
         src->head_dim != dst->head_dim)
         return fail(PCR_ERR_INVALID_ARG, "%s: host store and pool shapes differ", who);
-    if (method < PCR_LOAD_AUTO || method > PCR_LOAD_KERNEL_PULL)
+    if (method < PCR_LOAD_AUTO || method > PCR_LOAD_DMA_STAGED)
         return fail(PCR_ERR_INVALID_ARG, "%s: unknown method %d", who, (int)method);
     if (n == 0) return PCR_OK;
     if (!src_blocks || !dst_blocks) return fail(PCR_ERR_INVALID_ARG, "%s: NULL block list", who);
@@ -249,6 +305,15 @@ pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_b
     char *pv = static_cast<char *>(dst->v);
     if (method == PCR_LOAD_AUTO) method = PCR_LOAD_KERNEL_PULL;
 
+    if (method == PCR_LOAD_DMA_STAGED) {
+        st = check_workspace(ws, ws_bytes, n, bb, who);
+        if (st) return st;
+        st = staged_dma(const_cast<char *>(hk), const_cast<char *>(hv), static_cast<char *>(ws), src_blocks, n, bb,
+                        false, s, "pcr_load_kv_layer: hipMemcpyAsync");
+        if (st) return st;
+        return staged_kernel(dst, static_cast<char *>(ws), dst_blocks, n, bb, false, s,
+                             "pcr_load_kv_layer: scatter kernel launch");
+    }
     if (method == PCR_LOAD_DMA_PER_BLOCK) {
         for (int32_t i = 0; i < n; ++i) {
             hipError_t e = hipMemcpyAsync(pk + dst_blocks[i] * bb, hk + (int64_t)src_blocks[i] * bb, bb,
@@ -300,11 +365,207 @@ pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_b
     return PCR_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+pcr_status pcr_plan_offload(int32_t B, const int32_t *prefix_lens, const int32_t *suffix_lens,
+                            const int32_t *block_tables, int32_t max_blocks, int32_t block_size,
+                            int32_t chunk_tokens, int32_t first_dst_block,
+                            int32_t *src_blocks, int32_t *dst_blocks, int32_t cap, int32_t *n_pairs)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_plan_offload";
+    if (!n_pairs) return fail(PCR_ERR_INVALID_ARG, "%s: n_pairs is NULL", who);
+    *n_pairs = 0;
+    if (B < 0 || cap < 0 || first_dst_block < 0) return fail(PCR_ERR_INVALID_ARG, "%s: negative count", who);
+    if (B == 0) return PCR_OK;
+    if (!prefix_lens || !suffix_lens || !block_tables)
+        return fail(PCR_ERR_INVALID_ARG, "%s: NULL input array", who);
+    if (block_size <= 0 || chunk_tokens <= 0 || chunk_tokens % block_size)
+        return fail(PCR_ERR_INVALID_ARG, "%s: chunk_tokens %d is not a positive multiple of block_size %d", who,
+                    chunk_tokens, block_size);
+    const int64_t per_chunk = chunk_tokens / block_size;
+    int64_t k = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        const int64_t p = prefix_lens[b], s = suffix_lens[b];
+        if (p < 0 || s < 0) return fail(PCR_ERR_INVALID_ARG, "%s: sequence %d has a negative length", who, b);
+        const int64_t c0 = ceil_div(p, chunk_tokens), c1 = (p + s) / chunk_tokens;   // whole chunks in [p, p+s)
+        for (int64_t c = c0; c < c1; ++c) {
+            for (int64_t j = 0; j < per_chunk; ++j) {
+                const int64_t lb = c * per_chunk + j;
+                const int32_t blk = lb < max_blocks ? block_tables[(int64_t)b * max_blocks + lb] : -1;
+                if (blk < 0)
+                    return fail(PCR_ERR_INVALID_ARG, "%s: sequence %d logical block %lld has no pool block", who, b,
+                                (long long)lb);
+                if (k >= cap) return fail(PCR_ERR_INVALID_ARG, "%s: more than cap=%d pairs", who, cap);
+                if (first_dst_block + k > INT32_MAX)
+                    return fail(PCR_ERR_INVALID_ARG, "%s: host block ids overflow int32", who);
+                src_blocks[k] = blk;
+                dst_blocks[k] = (int32_t)(first_dst_block + k);
+                ++k;
+            }
+        }
+    }
+    *n_pairs = (int32_t)k;
+    return PCR_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+pcr_status offload_impl(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                        const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *ws, int64_t ws_bytes,
+                        void *stream)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_offload_kv_layer";
+    if (n < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n < 0", who);
+    if (!src || !dst) return fail(PCR_ERR_INVALID_ARG, "%s: NULL src or dst", who);
+    pcr_status st = check_pool(src, who);
+    if (st) return st;
+    if (!dst->k || !dst->v) return fail(PCR_ERR_INVALID_ARG, "%s: host k/v pointer is NULL", who);
+    st = check_layout(dst->block_size, dst->num_kv_heads, dst->head_dim, who);
+    if (st) return st;
+    if (src->block_size != dst->block_size || src->num_kv_heads != dst->num_kv_heads ||
+        src->head_dim != dst->head_dim)
+        return fail(PCR_ERR_INVALID_ARG, "%s: pool and host store shapes differ", who);
+    if (method < PCR_LOAD_AUTO || method > PCR_LOAD_DMA_STAGED)
+        return fail(PCR_ERR_INVALID_ARG, "%s: unknown method %d", who, (int)method);
+    if (n == 0) return PCR_OK;
+    if (!src_blocks || !dst_blocks) return fail(PCR_ERR_INVALID_ARG, "%s: NULL block list", who);
+    if (dst->num_blocks <= 0) return fail(PCR_ERR_INVALID_ARG, "%s: host store has no blocks", who);
+    {
+        std::vector<char> seen((size_t)dst->num_blocks, 0);
+        for (int32_t i = 0; i < n; ++i) {
+            if (src_blocks[i] < 0 || src_blocks[i] >= src->num_blocks)
+                return fail(PCR_ERR_INVALID_ARG, "%s: src block %d (pair %d) outside pool of %d", who, src_blocks[i],
+                            i, src->num_blocks);
+            if (dst_blocks[i] < 0 || dst_blocks[i] >= dst->num_blocks)
+                return fail(PCR_ERR_INVALID_ARG, "%s: dst block %d (pair %d) outside host store of %lld", who,
+                            dst_blocks[i], i, (long long)dst->num_blocks);
+            if (seen[dst_blocks[i]]++)
+                return fail(PCR_ERR_INVALID_ARG, "%s: dst block %d named twice", who, dst_blocks[i]);
+        }
+    }
+    const int64_t bb = block_bytes(src->block_size, src->num_kv_heads, src->head_dim);
+    const int64_t host_bytes = dst->num_blocks * bb;
+    void *dk = nullptr, *dv = nullptr;
+    st = check_pinned(dst->k, host_bytes, who, &dk);
+    if (st) return st;
+    st = check_pinned(dst->v, host_bytes, who, &dv);
+    if (st) return st;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *hk = static_cast<char *>(const_cast<void *>(dst->k));
+    char *hv = static_cast<char *>(const_cast<void *>(dst->v));
+    const char *pk = static_cast<const char *>(src->k);
+    const char *pv = static_cast<const char *>(src->v);
+    if (method == PCR_LOAD_AUTO) method = ws ? PCR_LOAD_DMA_STAGED : PCR_LOAD_KERNEL_PULL;
+    if (method == PCR_LOAD_DMA_STAGED) {
+        st = check_workspace(ws, ws_bytes, n, bb, who);
+        if (st) return st;
+        st = staged_kernel(src, static_cast<char *>(ws), src_blocks, n, bb, true, s,
+                           "pcr_offload_kv_layer: gather kernel launch");
+        if (st) return st;
+        return staged_dma(hk, hv, static_cast<char *>(ws), dst_blocks, n, bb, true, s,
+                          "pcr_offload_kv_layer: hipMemcpyAsync");
+    }
+    if (method == PCR_LOAD_DMA_PER_BLOCK) {
+        for (int32_t i = 0; i < n; ++i) {
+            hipError_t e = hipMemcpyAsync(hk + (int64_t)dst_blocks[i] * bb, pk + (int64_t)src_blocks[i] * bb, bb,
+                                          hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(hv + (int64_t)dst_blocks[i] * bb, pv + (int64_t)src_blocks[i] * bb, bb,
+                                   hipMemcpyDeviceToHost, s);
+            if (e != hipSuccess) return hip_fail(e, "pcr_offload_kv_layer: hipMemcpyAsync");
+        }
+        return PCR_OK;
+    }
+    if (method == PCR_LOAD_DMA_BATCH) {
+        memcpy_batch_fn batch = memcpy_batch();
+        if (!batch) return fail(PCR_ERR_UNSUPPORTED, "%s: this HIP runtime has no hipMemcpyBatchAsync", who);
+        std::vector<void *> dsts, srcs;
+        std::vector<size_t> sizes;
+        for (int kv = 0; kv < 2; ++kv) {
+            char *h = kv ? hv : hk;
+            const char *p = kv ? pv : pk;
+            int32_t i = 0;
+            while (i < n) {
+                int32_t j = i + 1;
+                while (j < n && src_blocks[j] == src_blocks[j - 1] + 1 && dst_blocks[j] == dst_blocks[j - 1] + 1) ++j;
+                dsts.push_back(h + (int64_t)dst_blocks[i] * bb);
+                srcs.push_back(const_cast<char *>(p) + (int64_t)src_blocks[i] * bb);
+                sizes.push_back((size_t)((j - i) * bb));
+                i = j;
+            }
+        }
+        size_t fail_idx = 0;
+        hipError_t e = batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), nullptr, nullptr, 0, &fail_idx, s);
+        if (e != hipSuccess) return hip_fail(e, "pcr_offload_kv_layer: hipMemcpyBatchAsync");
+        return PCR_OK;
+    }
+    for (int32_t off = 0; off < n; off += kPullPairsPerLaunch) {
+        PullArgs a;
+        a.n = std::min<int32_t>(kPullPairsPerLaunch, n - off);
+        memcpy(a.src, src_blocks + off, sizeof(int32_t) * a.n);
+        memcpy(a.dst, dst_blocks + off, sizeof(int32_t) * a.n);
+        hipError_t e = launch_push_blocks(src->k, src->v, src->num_blocks, dk, dv, dst->num_blocks, bb, a, s);
+        if (e != hipSuccess) return hip_fail(e, "pcr_offload_kv_layer: push kernel launch");
+    }
+    return PCR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pcr_status pcr_load_kv_layer_method(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
+                                    const int32_t *dst_blocks, int32_t n, pcr_load_method method,
+                                    void *copy_stream)
+{
+    if (method == PCR_LOAD_DMA_STAGED)
+        return fail(PCR_ERR_INVALID_ARG, "pcr_load_kv_layer: the staged method needs pcr_load_kv_layer_staged");
+    return load_impl(src, src_blocks, dst, dst_blocks, n, method, nullptr, 0, copy_stream);
+}
+
 pcr_status pcr_load_kv_layer(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
                              const int32_t *dst_blocks, int32_t n, void *copy_stream)
 {
-    return pcr_load_kv_layer_method(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_AUTO, copy_stream);
+    return load_impl(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_AUTO, nullptr, 0, copy_stream);
 }
+
+pcr_status pcr_load_kv_layer_staged(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
+                                    const int32_t *dst_blocks, int32_t n, void *workspace, int64_t workspace_bytes,
+                                    void *stream)
+{
+    return load_impl(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_DMA_STAGED, workspace, workspace_bytes, stream);
+}
+
+pcr_status pcr_offload_kv_layer_method(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                                       const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *stream)
+{
+    if (method == PCR_LOAD_DMA_STAGED)
+        return fail(PCR_ERR_INVALID_ARG,
+                    "pcr_offload_kv_layer: the staged method needs pcr_offload_kv_layer_staged");
+    return offload_impl(src, src_blocks, dst, dst_blocks, n, method, nullptr, 0, stream);
+}
+
+pcr_status pcr_offload_kv_layer(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                                const int32_t *dst_blocks, int32_t n, void *stream)
+{
+    return offload_impl(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_AUTO, nullptr, 0, stream);
+}
+
+pcr_status pcr_offload_kv_layer_staged(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                                       const int32_t *dst_blocks, int32_t n, void *workspace, int64_t workspace_bytes,
+                                       void *stream)
+{
+    return offload_impl(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_DMA_STAGED, workspace, workspace_bytes,
+                        stream);
+}
+
 
 pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void *v_new,
                          const int32_t *slot_mapping, int32_t T, void *stream)
@@ -392,3 +653,14 @@ pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, i
 }
 
 }  // extern "C"
+
+namespace pcr {
+
+pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
+                        const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *workspace,
+                        int64_t workspace_bytes, void *stream)
+{
+    return offload_impl(src, src_blocks, dst, dst_blocks, n, method, workspace, workspace_bytes, stream);
+}
+
+}  // namespace pcr

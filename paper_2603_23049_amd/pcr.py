@@ -26,12 +26,15 @@ LOAD_AUTO = 0
 LOAD_DMA_BATCH = 1
 LOAD_DMA_PER_BLOCK = 2
 LOAD_KERNEL_PULL = 3
+LOAD_DMA_STAGED = 4
 LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block": LOAD_DMA_PER_BLOCK,
-                "kernel_pull": LOAD_KERNEL_PULL}
+                "kernel_pull": LOAD_KERNEL_PULL, "dma_staged": LOAD_DMA_STAGED}
 
-EXPORTS = ["pcr_plan", "pcr_load_kv_layer", "pcr_load_kv_layer_method", "pcr_append_kv",
-           "pcr_prefix_prefill_attn", "pcr_gather_kv", "pcr_pipeline_run", "pcr_last_error",
-           "pcr_version"]
+EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_layer_method",
+           "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
+           "pcr_load_kv_layer_staged", "pcr_append_kv",
+           "pcr_prefix_prefill_attn", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
+           "pcr_last_error", "pcr_version"]
 
 
 class PcrError(RuntimeError):
@@ -86,6 +89,16 @@ def lib():
         L.pcr_gather_kv.argtypes = [ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, P, P, P]
         L.pcr_pipeline_run.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), ctypes.c_int, P, P,
                                        P]
+        L.pcr_plan_offload.argtypes = [i32, P, P, P, i32, i32, i32, i32, P, P, i32, P]
+        L.pcr_offload_kv_layer.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32, P]
+        L.pcr_offload_kv_layer_method.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32,
+                                                  ctypes.c_int, P]
+        L.pcr_offload_kv_layer_staged.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32, P, i64,
+                                                  P]
+        L.pcr_load_kv_layer_staged.argtypes = [ctypes.POINTER(_Host), P, ctypes.POINTER(_Pool), P, i32, P, i64, P]
+        L.pcr_pipeline_run_offload.argtypes = [ctypes.POINTER(_LayerIO), ctypes.POINTER(_Host), i32,
+                                               ctypes.POINTER(_Batch), P, P, i32, ctypes.c_int, ctypes.c_int, P,
+                                               i64, P, P, P, P]
         for name in EXPORTS:
             if name not in ("pcr_last_error", "pcr_version"):
                 getattr(L, name).restype = ctypes.c_int
@@ -192,14 +205,61 @@ def plan(prefix_lens: Sequence[int], suffix_lens: Sequence[int], block_tables, h
     return src[:n.value].copy(), dst[:n.value].copy(), slots[:T].copy(), cu
 
 
-def load_kv_layer(src: HostKV, src_blocks, dst: KVPool, dst_blocks, method: str = "auto", stream=None):
-    """pcr_load_kv_layer_method: enqueue the host-to-pool block copies on `stream`."""
+def load_kv_layer(src: HostKV, src_blocks, dst: KVPool, dst_blocks, method: str = "auto", stream=None,
+                  workspace=None):
+    """pcr_load_kv_layer_method (or _staged with method="dma_staged" and a device workspace
+    tensor): enqueue the host-to-pool block copies on `stream`."""
     sb, db = _i32_host(src_blocks), _i32_host(dst_blocks)
     if sb.shape != db.shape:
         raise ValueError("src_blocks and dst_blocks differ in length")
     h, p = src.c(), dst.c()
+    if method == "dma_staged":
+        ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+        _check(lib().pcr_load_kv_layer_staged(ctypes.byref(h), _ptr(sb), ctypes.byref(p), _ptr(db),
+                                              int(sb.shape[0]), _ptr(workspace), ws_bytes, _stream(stream)))
+        return
     _check(lib().pcr_load_kv_layer_method(ctypes.byref(h), _ptr(sb), ctypes.byref(p), _ptr(db), int(sb.shape[0]),
                                           LOAD_METHODS[method], _stream(stream)))
+
+
+def plan_offload(prefix_lens: Sequence[int], suffix_lens: Sequence[int], block_tables, block_size: int = 16,
+                 chunk_tokens: int = 256, first_dst_block: int = 0):
+    """pcr_plan_offload: returns (src pool blocks, dst host blocks) of the whole computed
+    chunks of every sequence, as int32 numpy arrays."""
+    pl, sl = _i32_host(prefix_lens), _i32_host(suffix_lens)
+    bt = _i32_host(block_tables)
+    B = int(pl.shape[0])
+    if bt.ndim != 2 or bt.shape[0] != B:
+        raise ValueError("block_tables must be [B][*]")
+    cap = int(sum((int(p) + int(s)) // block_size for p, s in zip(pl, sl)))
+    src = np.zeros(max(cap, 1), np.int32)
+    dst = np.zeros(max(cap, 1), np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib().pcr_plan_offload(B, _ptr(pl), _ptr(sl), _ptr(bt), bt.shape[1], block_size, chunk_tokens,
+                                  first_dst_block, _ptr(src), _ptr(dst), cap, ctypes.addressof(n)))
+    return src[:n.value].copy(), dst[:n.value].copy()
+
+
+def offload_kv_layer(src: KVPool, src_blocks, dst: HostKV, dst_blocks, method: str = "auto", stream=None,
+                     workspace=None):
+    """pcr_offload_kv_layer_method (or _staged with method="dma_staged" and a device
+    workspace tensor of at least 2 * n block bytes): pool-to-host block copies."""
+    sb, db = _i32_host(src_blocks), _i32_host(dst_blocks)
+    if sb.shape != db.shape:
+        raise ValueError("src_blocks and dst_blocks differ in length")
+    p, h = src.c(), dst.c()
+    if method == "dma_staged":
+        ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+        _check(lib().pcr_offload_kv_layer_staged(ctypes.byref(p), _ptr(sb), ctypes.byref(h), _ptr(db),
+                                                 int(sb.shape[0]), _ptr(workspace), ws_bytes, _stream(stream)))
+        return
+    _check(lib().pcr_offload_kv_layer_method(ctypes.byref(p), _ptr(sb), ctypes.byref(h), _ptr(db),
+                                             int(sb.shape[0]), LOAD_METHODS[method], _stream(stream)))
+
+
+def staged_workspace_bytes(n_blocks: int, num_kv_heads: int, head_dim: int, block_size: int = 16) -> int:
+    """Workspace the staged copies need for n_blocks blocks (K and V)."""
+    return 2 * n_blocks * block_size * num_kv_heads * head_dim * 2
 
 
 def append_kv(pool: KVPool, k_new, v_new, slot_mapping, stream=None):
@@ -284,3 +344,35 @@ def pipeline_run(layers: Sequence[Layer], batch: BatchPlan, copy_stream, compute
     per = t[:4 * n].reshape(n, 4)
     return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
             "end_ms": per[:, 3].copy(), "total_ms": float(t[4 * n]), "sum_compute_ms": float(t[4 * n + 1])}
+
+
+def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV], batch: BatchPlan, off_src, off_dst,
+                         copy_stream, compute_stream, offload_stream, method: str = "auto",
+                         offload_method: str = "auto", workspace=None, timing: bool = False):
+    """pcr_pipeline_run_offload: the three-stream pipeline. With timing=True, waits for the
+    last offload and returns per-layer load/compute/wait/offload ms and totals."""
+    n = len(layers)
+    if len(offload_dst) != n:
+        raise ValueError("one offload destination per layer")
+    arr = (_LayerIO * max(n, 1))()
+    for i, L in enumerate(layers):
+        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    dst = (_Host * max(n, 1))()
+    for i, h in enumerate(offload_dst):
+        dst[i] = h.c()
+    sb, db = _i32_host(off_src), _i32_host(off_dst)
+    if sb.shape != db.shape:
+        raise ValueError("off_src and off_dst differ in length")
+    b = batch.c()
+    t = np.zeros(6 * n + 3, np.float32) if timing else None
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(lib().pcr_pipeline_run_offload(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
+                                          LOAD_METHODS[method], LOAD_METHODS[offload_method], _ptr(workspace),
+                                          ws_bytes, _stream(copy_stream), _stream(compute_stream),
+                                          _stream(offload_stream), _ptr(t)))
+    if not timing:
+        return None
+    per = t[:6 * n].reshape(n, 6)
+    return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
+            "end_ms": per[:, 3].copy(), "offload_ms": per[:, 4].copy(), "offload_end_ms": per[:, 5].copy(),
+            "total_ms": float(t[6 * n]), "sum_compute_ms": float(t[6 * n + 1]), "compute_end_ms": float(t[6 * n + 2])}

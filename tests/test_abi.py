@@ -129,3 +129,25 @@ def test_argument_validation_before_any_device_work():
     lay = (pcr._LayerIO * 1)()
     bat = pcr._Batch()
     assert L.pcr_pipeline_run(lay, 1, P(bat), 0, 0x5, 0x5, None) == pcr.PCR_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("mk", [synth.tiny, synth.l8b_layer, synth.l70b_pipe80])
+def test_plan_offload_matches_oracle(mk):
+    b = mk()
+    for chunk in (16, 64, 256):
+        want = odm.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, 16, chunk, first_dst_block=3)
+        got = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, 16, chunk, first_dst_block=3)
+        for w, g in zip(want, got):
+            assert np.array_equal(w, g)
+
+
+def test_plan_offload_on_rag_mix_and_errors():
+    from paper_2603_23049_amd import prefix_tree
+    b = prefix_tree.rag_mix_batch()
+    want = odm.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables)
+    got = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables)
+    assert all(np.array_equal(w, g) for w, g in zip(want, got)) and len(got[0]) > 0
+    with pytest.raises(pcr.PcrError):
+        pcr.plan_offload([0], [64], np.array([[0, 1, 2, -1]], np.int32), 16, 64)   # missing pool block
+    with pytest.raises(pcr.PcrError):
+        pcr.plan_offload([0], [64], np.array([[0, 1, 2, 3]], np.int32), 16, 40)    # chunk not a block multiple

@@ -1,0 +1,145 @@
+"""GPU: pool-to-host offload of the computed chunks (Alg. 1 LayerwiseDownload), alone and
+as the third stream of the layer pipeline, bit for bit against the oracle.
+
+The host destination is filled with a marker pattern first: listed blocks must hold
+exactly the pool blocks after the layer's load + append, every other block must keep
+the marker. In the pipeline, each layer's offload must see that layer's finished
+append (it runs after the layer's compute), never stale pool bits.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2603_23049_amd import pcr, synth
+from gpuio import GpuLayer, pinned, say, u16
+from oracle import datamove as odm
+
+pytestmark = pytest.mark.gpu
+
+BS = 16
+MARK = np.uint16(0x5A5A)
+NAN_BITS = np.uint16(0x7FC1)
+
+
+def _host_out(b, n_blocks):
+    shape = (n_blocks, b.num_kv_heads, BS * b.head_dim)
+    return pcr.HostKV(pinned(np.full(shape, MARK, np.uint16)), pinned(np.full(shape, MARK, np.uint16)),
+                      b.num_kv_heads, b.head_dim)
+
+
+def _want(b, data, pk0, pv0, src, dst, n_blocks):
+    plan = odm.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, BS)
+    pk, pv = odm.pool_after_layer(pk0, pv0, data.host_k, data.host_v, plan, data.k_new, data.v_new, BS)
+    shape = (n_blocks, b.num_kv_heads, BS * b.head_dim)
+    hk, hv = np.full(shape, MARK, np.uint16), np.full(shape, MARK, np.uint16)
+    odm.offload(pk, pv, hk, hv, src, dst)
+    return hk, hv
+
+
+@pytest.mark.parametrize("method", ["kernel_pull", "dma_per_block", "dma_staged"])
+@pytest.mark.parametrize("chunk", [16, 64, 256])
+def test_offload_bitexact(method, chunk):
+    b = synth.ragged_batch("off", Hq=16, Hkv=4, d=128, prefix_lens=[0, 256, 48, 512], suffix_lens=[300, 256, 500, 40],
+                           pool_blocks=160, seed=21)
+    data = synth.make_layer(b)
+    rng = np.random.Generator(np.random.PCG64(22))
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    pk0, pv0 = synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
+    src, dst = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, BS, chunk, first_dst_block=2)
+    assert len(src) > 0
+    n_blocks = int(dst.max()) + 3
+    say(f"[gpu] offload chunk={chunk} method={method} blocks={len(src)}")
+    L = GpuLayer(b, data, pk0, pv0)
+    L.run_serial("kernel_pull")
+    host = _host_out(b, n_blocks)
+    ws = torch.empty(pcr.staged_workspace_bytes(len(src), b.num_kv_heads, b.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    # reversed host order too: the staged copies then have one run per block
+    order = slice(None, None, -1) if chunk == 64 else slice(None)
+    pcr.offload_kv_layer(L.pool, src[order], host, dst[order], method=method, workspace=ws)
+    torch.cuda.synchronize()
+    hk, hv = _want(b, data, pk0, pv0, src, dst, n_blocks)
+    assert np.array_equal(u16(host.k), hk)
+    assert np.array_equal(u16(host.v), hv)
+
+
+def test_offload_rejects_pageable_and_bad_ids():
+    b = synth.tiny()
+    data = synth.make_layer(b)
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    z = np.zeros(shape, np.uint16)
+    L = GpuLayer(b, data, z, z)
+    pageable = pcr.HostKV(torch.zeros((4, b.num_kv_heads, BS * b.head_dim), dtype=torch.int16),
+                          torch.zeros((4, b.num_kv_heads, BS * b.head_dim), dtype=torch.int16), b.num_kv_heads,
+                          b.head_dim)
+    with pytest.raises(pcr.PcrError) as e:
+        pcr.offload_kv_layer(L.pool, [0], pageable, [0])
+    assert e.value.status == pcr.PCR_ERR_NOT_PINNED
+    host = _host_out(b, 4)
+    with pytest.raises(pcr.PcrError):
+        pcr.offload_kv_layer(L.pool, [b.pool_blocks], host, [0])        # src outside the pool
+    with pytest.raises(pcr.PcrError):
+        pcr.offload_kv_layer(L.pool, [0, 1], host, [2, 2])              # dst named twice
+    ws = torch.empty(1024, dtype=torch.uint8, device="cuda")
+    with pytest.raises(pcr.PcrError):
+        pcr.offload_kv_layer(L.pool, [0, 1], host, [0, 1], method="dma_staged", workspace=ws)   # too small
+    with pytest.raises(pcr.PcrError):
+        pcr.offload_kv_layer(L.pool, [0], host, [0], method="dma_staged")                       # no workspace
+    pcr.offload_kv_layer(L.pool, [], host, [])                          # empty: no-op
+    torch.cuda.synchronize()
+    assert np.all(u16(host.k) == MARK)
+
+
+@pytest.mark.parametrize("method", ["kernel_pull", "dma_per_block", "dma_staged"])
+def test_pipeline_with_offload_bitwise(method):
+    n = 5
+    b = synth.uniform_batch("pipe_off", B=2, Hq=32, Hkv=8, d=128, p=1024, s=520, pool_blocks=512, seed=3,
+                            num_layers=n, layer_seed_base=3100)
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    poison = np.full(shape, NAN_BITS, np.uint16)
+    layers = [GpuLayer(b, synth.make_layer(b, l), poison, poison) for l in range(n)]
+    src, dst = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, BS, 256)
+    assert len(src) == 2 * 2 * 16          # chunks 4 and 5 of each sequence
+    n_blocks = len(src)
+    outs = [_host_out(b, n_blocks) for _ in range(n)]
+    say(f"[gpu] pipeline with offload, {n} layers, method={method}")
+    load_method = "kernel_pull" if method == "dma_staged" else method
+    ws = torch.empty(pcr.staged_workspace_bytes(len(src), b.num_kv_heads, b.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    serial = []
+    for L in layers:
+        L.run_serial(load_method)
+        serial.append(u16(L.out).copy())
+        L.pool.k.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.pool.v.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.out.zero_()
+    torch.cuda.synchronize()
+    cs, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    t = pcr.pipeline_run_offload([L.layer_io() for L in layers], outs, layers[0].batch_plan(), src, dst, cs, ks,
+                                 os_, method=load_method, offload_method=method, workspace=ws, timing=True)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        assert np.array_equal(u16(L.out), serial[l]), f"layer {l}: output differs from serial"
+        hk, hv = _want(b, synth.make_layer(b, l), poison, poison, src, dst, n_blocks)
+        assert np.array_equal(u16(outs[l].k), hk), f"layer {l}: offloaded K"
+        assert np.array_equal(u16(outs[l].v), hv), f"layer {l}: offloaded V"
+    assert np.all(t["offload_ms"] > 0) and t["total_ms"] >= t["compute_end_ms"] > 0
+    assert np.all(t["offload_end_ms"][1:] >= t["offload_end_ms"][:-1])
+
+
+def test_staged_load_bitexact():
+    b = synth.ragged_batch("ld", Hq=16, Hkv=4, d=128, prefix_lens=[512, 48, 0, 300], suffix_lens=[10, 20, 30, 1],
+                           pool_blocks=100, seed=23)
+    data = synth.make_layer(b)
+    rng = np.random.Generator(np.random.PCG64(24))
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    pk0, pv0 = synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
+    L = GpuLayer(b, data, pk0, pv0)
+    ws = torch.empty(pcr.staged_workspace_bytes(len(L.src), b.num_kv_heads, b.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    say(f"[gpu] staged load, {len(L.src)} blocks")
+    pcr.load_kv_layer(L.host, L.src, L.pool, L.dst, method="dma_staged", workspace=ws)
+    torch.cuda.synchronize()
+    pk, pv = pk0.copy(), pv0.copy()
+    odm.load(pk, pv, data.host_k, data.host_v, L.src, L.dst)
+    assert np.array_equal(u16(L.pool.k), pk) and np.array_equal(u16(L.pool.v), pv)

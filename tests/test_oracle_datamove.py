@@ -115,3 +115,48 @@ def test_slot_mapping_brute_force_tiny_config():
     assert list(dst) == list(bt[:16]) and list(src) == list(range(16))
     # token 256+i sits in logical block 16 + i//16 at offset i%16
     assert list(slots) == [int(bt[16 + i // 16]) * 16 + i % 16 for i in range(64)]
+
+
+def test_plan_offload_lists_exactly_the_computed_whole_chunks():
+    """Brute force over tokens: a pool block is offloaded iff all tokens of its chunk are
+    computed tokens of the sequence; order follows the sequences and positions."""
+    bs, chunk = 16, 64
+    prefix_lens = [0, 64, 70, 128, 0]
+    suffix_lens = [200, 64, 130, 10, 63]
+    rng = np.random.Generator(np.random.PCG64(11))
+    need = [-(-(p + s) // bs) for p, s in zip(prefix_lens, suffix_lens)]
+    perm = rng.permutation(sum(need)).astype(np.int32)
+    bt = np.full((len(need), max(need)), -1, np.int32)
+    off = 0
+    for b, n in enumerate(need):
+        bt[b, :n] = perm[off:off + n]
+        off += n
+    src, dst = dm.plan_offload(prefix_lens, suffix_lens, bt, bs, chunk, first_dst_block=5)
+    want = []
+    for b, (p, s) in enumerate(zip(prefix_lens, suffix_lens)):
+        for lb in range(-(-(p + s) // bs)):
+            c = (lb * bs) // chunk
+            tokens = range(c * chunk, (c + 1) * chunk)
+            if all(p <= t < p + s for t in tokens):
+                want.append(int(bt[b, lb]))
+    assert src.tolist() == want
+    assert dst.tolist() == list(range(5, 5 + len(want)))
+    # 0+200: chunks 0,1,2 (192 tokens); 64+64: chunk 1; 70+130: chunk 2 (128..191); 128+10: none; 0+63: none
+    assert len(want) == (3 + 1 + 1) * (chunk // bs)
+
+
+def test_offload_then_load_round_trip():
+    rng = np.random.Generator(np.random.PCG64(12))
+    pool_k = rng.integers(0, 65536, size=(20, 2, 64), dtype=np.uint16)
+    pool_v = rng.integers(0, 65536, size=(20, 2, 64), dtype=np.uint16)
+    host_k = np.zeros((6, 2, 64), np.uint16)
+    host_v = np.zeros((6, 2, 64), np.uint16)
+    src = [7, 3, 19, 0, 11, 12]
+    dm.offload(pool_k, pool_v, host_k, host_v, src, range(6))
+    back_k, back_v = np.zeros_like(pool_k), np.zeros_like(pool_v)
+    dm.load(back_k, back_v, host_k, host_v, range(6), src)
+    for i, s in enumerate(src):
+        assert np.array_equal(back_k[s], pool_k[s]) and np.array_equal(back_v[s], pool_v[s])
+        assert np.array_equal(host_k[i], pool_k[s])
+    untouched = [b for b in range(20) if b not in src]
+    assert not back_k[untouched].any()
