@@ -290,6 +290,40 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
             "exposed_ideal_ms_per_layer": load_ms_iso / n if compute_ms_iso >= load_ms_iso else None}
 
 
+def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
+    """One decode step (one new token per sequence, attending over ctx cached keys) of a
+    Llama-3-8B-shaped batch, attention only; pool, Q and tables drawn on the device (the
+    values do not change the work). HBM bytes = every key's K and V once + Q + out."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    bs = 16
+    nb = -(-ctx // bs)
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    pool_blocks = B * nb
+    pk = torch.randn((pool_blocks, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+    pv = torch.randn((pool_blocks, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+    pool = pcr.KVPool(pk, pv, Hkv, d)
+    bt = torch.randperm(pool_blocks, device="cuda", generator=g).to(torch.int32).view(B, nb)
+    q = torch.randn((B, Hq, d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+    out = torch.empty_like(q)
+    pl_h = np.full(B, ctx - 1, np.int32)
+    cu_h = np.arange(B + 1, dtype=np.int32)
+    pl, cu = torch.from_numpy(pl_h).cuda(), torch.from_numpy(cu_h).cuda()
+    s = torch.cuda.current_stream()
+    for _ in range(3):
+        pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)
+    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(steps):
+        pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)
+    e.record(s)
+    e.synchronize()
+    ms = a.elapsed_time(e) / steps
+    nbytes = B * ctx * Hkv * d * 2 * 2 + 2 * B * Hq * d * 2
+    return {"workload": f"decode B={B} ctx={ctx} Hq={Hq} Hkv={Hkv} d={d}", "attn_ms": ms, "hbm_bytes": nbytes,
+            "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3}
+
+
 def flow_shop3_makespan(load_ms: float, compute_ms: float, offload_ms: float, n: int) -> float:
     """Least makespan of n identical layers through three in-order queues (load, then
     compute, then offload): one layer's three steps plus n-1 times the slowest step."""
@@ -464,6 +498,8 @@ def main(argv=None):
         pipelines[pbatch.name] = pipe
     extra = {}
     if not args.no_extra:
+        _say("[bench] decode step")
+        extra["decode"] = measure_decode()
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
         rst = measure_step(rb, max(10, args.steps // 2), 3)
@@ -527,6 +563,7 @@ def main(argv=None):
         "pipelines": pipelines or None,
         "rag_mix": extra.get("rag_mix"),
         "offload": extra.get("offload"),
+        "decode": extra.get("decode"),
         "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
         "cpu_baseline": cpu,
         "wall_s_timed": st["wall_s"],
