@@ -324,6 +324,50 @@ def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
             "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3}
 
 
+def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_chunks=96, request_compute_ms=30.0, n_serve=40):
+    """Serving loop through DRAM and SSD tiers with the queue-window prefetch: SSD stall
+    per request for each window size, on this machine's disk (O_DIRECT when the file
+    system allows it). Chunks are scaled to chunk_mib MiB; compute is a sleep of
+    request_compute_ms per 2500 computed tokens."""
+    import shutil
+    import tempfile
+    from paper_2603_23049_amd import prefetch, synth
+    stream = synth.rag_stream(4, n_requests=64 + n_serve)
+    base = os.path.join(ROOT, ".pytest_store")
+    os.makedirs(base, exist_ok=True)
+    d = tempfile.mkdtemp(dir=base)
+    out = {"chunk_bytes": chunk_mib << 20, "dram_chunks": dram_chunks, "requests": n_serve,
+           "compute_ms_per_2500_tokens": request_compute_ms}
+    try:
+        for w in windows:
+            st = prefetch.serve(stream.requests, store_path=os.path.join(d, f"w{w}.bin"), chunk_bytes=chunk_mib << 20,
+                                dram_chunks=dram_chunks, window=w, compute_ms_per_token=request_compute_ms / 2500,
+                                io_threads=4)
+            out[f"window_{w}"] = {"stall_ms_per_request": st.stall_ms / max(st.requests, 1),
+                                  "on_demand_reads": st.on_demand_reads, "prefetch_reads": st.prefetch_reads,
+                                  "prefetch_hits": st.prefetch_hits, "dram_hits": st.dram_hits,
+                                  "wall_ms": st.wall_ms}
+        probe = prefetch.page_aligned_buffer(chunk_mib << 20)
+        from paper_2603_23049_amd import pcr
+        store = pcr.ChunkStore(os.path.join(d, "probe.bin"), chunk_mib << 20, 4)
+        bufs = [prefetch.page_aligned_buffer(chunk_mib << 20) for _ in range(16)]
+        for i, b in enumerate(bufs):
+            store.write_async(i, b)
+        store.wait()
+        t0 = time.perf_counter()
+        for i, b in enumerate(bufs):
+            store.read_async(i, b)
+        store.wait()
+        dt = time.perf_counter() - t0
+        out["ssd_read_GBps"] = 16 * (chunk_mib << 20) / dt / 1e9
+        out["direct_io"] = store.stats()["direct_io"]
+        store.close()
+        del probe
+    finally:
+        shutil.rmtree(d, ignore_errors=True)
+    return out
+
+
 def flow_shop3_makespan(load_ms: float, compute_ms: float, offload_ms: float, n: int) -> float:
     """Least makespan of n identical layers through three in-order queues (load, then
     compute, then offload): one layer's three steps plus n-1 times the slowest step."""
@@ -498,6 +542,8 @@ def main(argv=None):
         pipelines[pbatch.name] = pipe
     extra = {}
     if not args.no_extra:
+        _say("[bench] SSD tier: queue-window prefetch")
+        extra["prefetch"] = measure_prefetch()
         _say("[bench] decode step")
         extra["decode"] = measure_decode()
         rb = workload("rag_mix")
@@ -564,6 +610,7 @@ def main(argv=None):
         "rag_mix": extra.get("rag_mix"),
         "offload": extra.get("offload"),
         "decode": extra.get("decode"),
+        "prefetch": extra.get("prefetch"),
         "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
         "cpu_baseline": cpu,
         "wall_s_timed": st["wall_s"],

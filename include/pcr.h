@@ -320,6 +320,33 @@ pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_k
                                     void *copy_stream, void *compute_stream, void *offload_stream,
                                     float *timing_ms);
 
+/*
+ * The SSD tier of the chunk cache (Sec. 4.4 queue-based prefetch and asynchronous
+ * write-back; Sec. 5 dedicated prefetch thread). A store is one file of fixed-size
+ * chunk slots (chunk id c at byte c * chunk_bytes) served by io_threads host
+ * threads in submission order. The file is created (truncated) at open. Buffers
+ * belong to the caller and must stay untouched until the chunk's task completes;
+ * page-aligned buffers (e.g. pinned host memory) with a page-multiple chunk size
+ * bypass the page cache (O_DIRECT). No GPU work is involved.
+ *   pcr_store_write_async   queue chunk_bytes from src as chunk chunk_id
+ *   pcr_store_read_async    queue a read of chunk chunk_id into dst; first waits for
+ *                           earlier writes of that chunk; PCR_ERR_INVALID_ARG if the
+ *                           chunk was never written
+ *   pcr_store_wait          block until chunk_id's tasks (or, for chunk_id < 0, all
+ *                           tasks) are done; reports the first I/O error, if any
+ *   pcr_store_poll          *done = 1 if nothing is pending for chunk_id (or at all)
+ *   pcr_store_stats         bytes moved so far, and whether O_DIRECT is in use
+ *   pcr_store_close         drain the queue, stop the threads, close the file
+ */
+typedef struct pcr_chunk_store pcr_chunk_store;
+pcr_status pcr_store_open(const char *path, int64_t chunk_bytes, int32_t io_threads, pcr_chunk_store **out);
+pcr_status pcr_store_write_async(pcr_chunk_store *store, int64_t chunk_id, const void *src);
+pcr_status pcr_store_read_async(pcr_chunk_store *store, int64_t chunk_id, void *dst);
+pcr_status pcr_store_wait(pcr_chunk_store *store, int64_t chunk_id);
+pcr_status pcr_store_poll(pcr_chunk_store *store, int64_t chunk_id, int32_t *done);
+pcr_status pcr_store_stats(pcr_chunk_store *store, int64_t *bytes_read, int64_t *bytes_written, int32_t *direct);
+pcr_status pcr_store_close(pcr_chunk_store *store);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *pcr_last_error(void);
 

@@ -34,7 +34,8 @@ EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_lay
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
            "pcr_prefix_prefill_attn", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
-           "pcr_last_error", "pcr_version"]
+           "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
+           "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
 
 
 class PcrError(RuntimeError):
@@ -99,6 +100,13 @@ def lib():
         L.pcr_pipeline_run_offload.argtypes = [ctypes.POINTER(_LayerIO), ctypes.POINTER(_Host), i32,
                                                ctypes.POINTER(_Batch), P, P, i32, ctypes.c_int, ctypes.c_int, P,
                                                i64, P, P, P, P]
+        L.pcr_store_open.argtypes = [ctypes.c_char_p, i64, i32, ctypes.POINTER(ctypes.c_void_p)]
+        L.pcr_store_write_async.argtypes = [P, i64, P]
+        L.pcr_store_read_async.argtypes = [P, i64, P]
+        L.pcr_store_wait.argtypes = [P, i64]
+        L.pcr_store_poll.argtypes = [P, i64, P]
+        L.pcr_store_stats.argtypes = [P, P, P, P]
+        L.pcr_store_close.argtypes = [P]
         for name in EXPORTS:
             if name not in ("pcr_last_error", "pcr_version"):
                 getattr(L, name).restype = ctypes.c_int
@@ -376,3 +384,59 @@ def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV],
     return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
             "end_ms": per[:, 3].copy(), "offload_ms": per[:, 4].copy(), "offload_end_ms": per[:, 5].copy(),
             "total_ms": float(t[6 * n]), "sum_compute_ms": float(t[6 * n + 1]), "compute_end_ms": float(t[6 * n + 2])}
+
+
+class ChunkStore:
+    """The SSD tier: a file of fixed-size chunk slots with asynchronous reads and writes
+    served by native I/O threads (pcr_store_*). Buffers are numpy arrays or host
+    tensors of exactly chunk_bytes, kept alive until their chunk's task completes."""
+
+    def __init__(self, path: str, chunk_bytes: int, io_threads: int = 4):
+        self.chunk_bytes = int(chunk_bytes)
+        h = ctypes.c_void_p()
+        _check(lib().pcr_store_open(os.fsencode(path), self.chunk_bytes, int(io_threads), ctypes.byref(h)))
+        self._h = h
+        self._keep = {}
+
+    def _buf(self, buf):
+        n = buf.nbytes if isinstance(buf, np.ndarray) else buf.numel() * buf.element_size()
+        if n != self.chunk_bytes:
+            raise ValueError(f"buffer of {n} bytes, chunk is {self.chunk_bytes}")
+        return _ptr(buf)
+
+    def write_async(self, chunk_id: int, src):
+        self._keep.setdefault(int(chunk_id), []).append(src)
+        _check(lib().pcr_store_write_async(self._h, int(chunk_id), self._buf(src)))
+
+    def read_async(self, chunk_id: int, dst):
+        self._keep.setdefault(int(chunk_id), []).append(dst)
+        _check(lib().pcr_store_read_async(self._h, int(chunk_id), self._buf(dst)))
+
+    def wait(self, chunk_id: int = -1):
+        _check(lib().pcr_store_wait(self._h, int(chunk_id)))
+        if chunk_id < 0:
+            self._keep.clear()
+        else:
+            self._keep.pop(int(chunk_id), None)
+
+    def done(self, chunk_id: int = -1) -> bool:
+        d = ctypes.c_int32(0)
+        _check(lib().pcr_store_poll(self._h, int(chunk_id), ctypes.addressof(d)))
+        return bool(d.value)
+
+    def stats(self):
+        r, w, d = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int32(0)
+        _check(lib().pcr_store_stats(self._h, ctypes.addressof(r), ctypes.addressof(w), ctypes.addressof(d)))
+        return {"bytes_read": r.value, "bytes_written": w.value, "direct_io": bool(d.value)}
+
+    def close(self):
+        if self._h:
+            h, self._h = self._h, None
+            _check(lib().pcr_store_close(h))
+            self._keep.clear()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
