@@ -90,6 +90,9 @@ struct TileGeom {
 };
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// s_waitcnt immediate that waits for LDS, scalar-memory and message counters only
+// (lgkmcnt = 0; vmcnt and expcnt at their maxima, so they do not wait).
+constexpr int kWaitLgkm0 = 0xC07F;
 
 // Workgroup barrier without a memory fence. The phase schedule orders its memory
 // traffic explicitly: every direct load is waited for (vmcnt) by the wave that
@@ -139,13 +142,18 @@ __device__ __forceinline__ void wait_vmem_keep()
 // host from the sequence lengths and passed by value in the kernel arguments.
 // Sequences are taken heaviest first (longest key range), and inside a sequence the
 // last row tiles (the most keys) first, so the long items start early and the
-// short ones fill the tail.
+// short ones fill the tail. Each slot also carries its sequence's lengths, so a
+// workgroup finds everything it needs about its sequence in one parallel read of
+// the map (the kernel arguments) instead of a chain of dependent loads.
 constexpr int kMaxMapSeqs = 128;
 struct AttnWorkMap {
     int32_t n_seq;                      // sequences with rows; 0: plain (b, g, rt) order
     int32_t per_head;                   // row tiles of all sequences, one kv head
-    int32_t order[kMaxMapSeqs];         // sequence in each slot
-    int32_t cum[kMaxMapSeqs + 1];       // row tiles before each slot
+    int32_t seq[kMaxMapSeqs];           // sequence in each slot
+    int32_t tiles_end[kMaxMapSeqs];     // row tiles of the slots up to and including this one
+    int32_t prefix[kMaxMapSeqs];        // the slot's cached tokens p
+    int32_t first[kMaxMapSeqs];         // the slot's first new token (row of q and out)
+    int32_t count[kMaxMapSeqs];         // the slot's new tokens s
 };
 
 template <int D>
@@ -172,7 +180,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // kv head), which read the same K/V, go to workgroups of one XCD and share its L2.
     // With the work map and Hkv a multiple of 8, XCD x takes kv heads x, x+8, ... of
     // every sequence, so the eight XCDs get equal work.
-    int b, g, rt;
+    const int tid = threadIdx.x, lane = tid & 63;
+    int b, g, rt, p, t0, s;
     {
         const int x = (int)(blockIdx.x % kXcds), i = (int)(blockIdx.x / kXcds);
         const int per_xcd = (int)(gridDim.x / kXcds);
@@ -188,13 +197,28 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 j = w - g * wm.per_head;
             }
             if (g >= Hkv) return;
-            int lo = 0, hi = wm.n_seq - 1;               // slot with cum[lo] <= j < cum[lo + 1]
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (wm.cum[mid] <= j) lo = mid; else hi = mid - 1;
+            // Slot of row tile j: the number of slots whose tiles end at or before j. Lane l
+            // reads slots l and l + 64 (all fields at once); the slot's fields are then taken
+            // from the lane that holds them.
+            int e[2], fs[2], fp[2], ft[2], fc[2];
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const int k = lane + 64 * hf;
+                const bool in = k < wm.n_seq;
+                e[hf] = in ? wm.tiles_end[k] : INT32_MAX;
+                fs[hf] = in ? wm.seq[k] : 0;
+                fp[hf] = in ? wm.prefix[k] : 0;
+                ft[hf] = in ? wm.first[k] : 0;
+                fc[hf] = in ? wm.count[k] : 0;
             }
-            b = wm.order[lo];
-            rt = wm.cum[lo + 1] - 1 - j;
+            const int slot = __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[0] <= j)) +
+                             __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[1] <= j));
+            const int hf = slot >> 6, sl = slot & 63;
+            b = __builtin_amdgcn_readlane(hf ? fs[1] : fs[0], sl);
+            p = __builtin_amdgcn_readlane(hf ? fp[1] : fp[0], sl);
+            t0 = __builtin_amdgcn_readlane(hf ? ft[1] : ft[0], sl);
+            s = __builtin_amdgcn_readlane(hf ? fc[1] : fc[0], sl);
+            rt = __builtin_amdgcn_readlane(hf ? e[1] : e[0], sl) - 1 - j;
         } else {
             const int n_work = row_tiles * Hkv * B;
             const int w = x * per_xcd + i;
@@ -202,21 +226,20 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             rt = w % row_tiles;
             g = (w / row_tiles) % Hkv;
             b = w / (row_tiles * Hkv);
+            p = prefix_lens[b];
+            t0 = cu_suffix[b];
+            s = cu_suffix[b + 1] - t0;
         }
     }
-    const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2;              // 0: first half of the keys, 1: second half
     const int wg = wave & 3;                // wave within the group (selects the rows)
     const int qc = lane & 31, half = lane >> 5;
 
-    const int p = prefix_lens[b];
-    const int t0 = cu_suffix[b];
-    const int s = cu_suffix[b + 1] - t0;
     const int G = Hq / Hkv;
     const int rows_total = s * G;
     const int row0 = rt * kRowsPerWG;
-    if (s <= 0 || row0 >= rows_total) return;   // uniform over the workgroup
+    if (s <= 0 || row0 >= rows_total || T <= 0) return;   // uniform over the workgroup
     const int total = p + s;
 
     // This lane's packed query row (rows past the end compute a copy of the last row).
@@ -237,22 +260,17 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int w_min_limit = p + w_first / G;
     const int valid_blocks = min((total + kBlockSize - 1) / kBlockSize, max_blocks);
 
-    // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row),
-    // pre-multiplied by sm_scale*log2(e) so that the first product yields log2-domain
-    // scores directly.
-    bf16x8 qf[KSTEPS];
+    // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row). The
+    // loads go out here; the scaling waits until the first K tile has been requested.
+    // All eight loads are unconditional, so that they are in flight together (a row past
+    // the end reads row 0 of head 0, which exists since T > 0, and is zeroed later).
+    const bool q_ok = tq < T;
+    u32x4 q_raw[KSTEPS];
+    bf16x8 qf[KSTEPS];    // the Q^T operand, set once K(0) has been requested
     {
-        const bool ok = tq < T;
-        const u16 *qrow = q + (ok ? (tq * Hq + h) * D : 0);
+        const u16 *qrow = q + (q_ok ? (tq * Hq + h) * D : 0);
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (ok) v = *reinterpret_cast<const u32x4 *>(qrow + 16 * ks + 8 * half);
-            f32x8 f = __builtin_convertvector(as_bf16x8(v), f32x8);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) f[e] *= scale_log2;
-            qf[ks] = __builtin_convertvector(f, bf16x8);
-        }
+        for (int ks = 0; ks < KSTEPS; ++ks) q_raw[ks] = *reinterpret_cast<const u32x4 *>(qrow + 16 * ks + 8 * half);
     }
 
     f32x16 o_acc[MT];
@@ -280,17 +298,16 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     auto vbuf_off = [&](int j) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
 
     // Pool block ids of this group's tile j, read raw (as scalars) one phase before
-    // use. Logical blocks past the sequence read the last valid entry (so the loads
-    // need no branch) and become block 0. The range check happens at use, so the
-    // scalar loads are never waited for on the spot: an id past the sequence or
-    // outside the pool becomes block 0 (its keys are masked and its V entries cleared
-    // before use), so no load ever leaves the pool.
+    // use. Logical blocks past the sequence read the last valid entry, so the four loads
+    // are independent and nothing consumes their values until the range check at use:
+    // every key past the sequence is masked and the V entries past it are cleared in
+    // the last tile, so any in-pool block can stand in there; an id outside the pool
+    // becomes block 0, so no load ever leaves the pool.
     auto tile_ids = [&](int j, int32_t (&ids)[kTileBlocks]) {
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) {
             const int lb = (tile_begin + j) * kTileBlocks + jb;
-            const int32_t v = bt[min(lb, valid_blocks - 1)];
-            ids[jb] = lb < valid_blocks ? v : 0;
+            ids[jb] = bt[min(lb, valid_blocks - 1)];
         }
     };
     // Byte offset of the (pool block, kv head g) payload of a raw block id; an id outside
@@ -304,6 +321,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) offs[jb] = payload_off(ids[jb]);
     };
+    int32_t ids_raw[kTileBlocks];   // ids of the tile two ahead, read in a vector cluster
     // Direct-load addressing. A tile's K (or V) is 4 pool blocks of one kv head, each a
     // contiguous payload of kSlabs 1 KB slabs; wave wg loads slabs u*4 + wg. Because 4
     // is a multiple of kSlabs, a lane's byte offset inside the payload is the same for
@@ -367,9 +385,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // behind the MFMAs). When QK runs, the cluster also issues the direct loads of
     // V(j+1) and K(j+2), one per few MFMAs, so the texture path never backs up a wave.
     auto matrix_cluster = [&](auto pv_tag, auto qk_tag, int j, const bf16x8 (&pf)[kTileBlocks],
-                              f32x16 (&st)[2], const int64_t (&idv)[kTileBlocks],
-                              const int64_t (&idk)[kTileBlocks]) {
+                              f32x16 (&st)[2], int64_t (&idv)[kTileBlocks], int64_t (&idk)[kTileBlocks],
+                              auto convert_tag) {
         constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
+
         constexpr int NPV = DO_PV ? kTileBlocks * MT : 0, NQK = DO_QK ? 2 * KSTEPS : 0, NALL = NPV + NQK;
         constexpr int NLD = DO_QK ? kVLoads + kKLoads : 0;
         constexpr int NLD1 = NLD > 0 ? NLD : 1;
@@ -396,6 +415,17 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         u32x4 fr[NALL];
 #pragma unroll
         for (int i = 0; i < kAhead && i < NALL; ++i) fr[i] = frag(i);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (decltype(convert_tag)::value) {
+            // Block ids read in the preceding vector cluster (and waited for at its end)
+            // become payload offsets here, while the first fragment reads are in flight.
+#pragma unroll
+            for (int jb = 0; jb < kTileBlocks; ++jb) {
+                idv[jb] = idk[jb];
+                idk[jb] = payload_off(ids_raw[jb]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
         int ld = 0;
 #pragma unroll
         for (int i = 0; i < NALL; ++i) {
@@ -414,9 +444,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 ++ld;
             }
         }
-        // keep that schedule: the first reads, then (read, MFMA[, load]) groups, then the last MFMAs
-#pragma unroll
-        for (int i = 0; i < kAhead && i < NALL; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        // keep that schedule: (read, MFMA[, load]) groups, then the last MFMAs
 #pragma unroll
         for (int i = 0; i < NALL; ++i) {
             if (i + kAhead < NALL) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
@@ -497,12 +525,21 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // Block offsets travel one phase ahead: at C(j), ids_v holds tile j+1's (for
     // V(j+1)) and ids_k tile j+2's (for K(j+2)).
     int64_t ids_v[kTileBlocks], ids_k[kTileBlocks];   // payload byte offsets
-    int32_t ids_raw[kTileBlocks];
     tile_ids(0, ids_raw);
     to_offs(ids_raw, ids_v);
     if (n > 0) issue_k(0, ids_v);                      // K(0) for C(-1)
     tile_ids(1, ids_raw);
     to_offs(ids_raw, ids_k);
+    // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row),
+    // pre-multiplied by sm_scale*log2(e) so that the first product yields log2-domain
+    // scores directly.
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+        f32x8 f = __builtin_convertvector(as_bf16x8(q_ok ? q_raw[ks] : u32x4{0u, 0u, 0u, 0u}), f32x8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] *= scale_log2;
+        qf[ks] = __builtin_convertvector(f, bf16x8);
+    }
     wait_vmem();
     __syncthreads();
 
@@ -513,18 +550,19 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         phase_barrier();
         ++ph;
     };
-    // M(j): softmax of tile j; block ids of tile j+2 (read now, range-checked at the
-    // end, when they have long arrived); then wait for the loads C(j-1) issued.
+    // M(j): softmax of tile j; block ids of tile j+2 (read now, range-checked and
+    // converted at the start of C(j)); then wait for the loads C(j-1) issued.
     auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+        // The scalar loads of the ids go out before the softmax, whose length covers
+        // their latency (left to itself the scheduler sinks them next to their use).
         tile_ids(j + 2, ids_raw);
+        __builtin_amdgcn_sched_barrier(0);
         softmax(j, st, pf);
-        __builtin_amdgcn_sched_barrier(0);   // the id conversion waits for the scalar loads: keep it last
-#pragma unroll
-        for (int jb = 0; jb < kTileBlocks; ++jb) {
-            ids_v[jb] = ids_k[jb];
-            ids_k[jb] = payload_off(ids_raw[jb]);
-        }
         wait_vmem();
+        // The id loads landed long ago; an explicit wait here (seen by the compiler) keeps
+        // it from placing one among the next matrix cluster's fragment reads.
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     };
 
     f32x16 st[2];
@@ -532,20 +570,20 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     if (grp == 1) phase_end();
     if (n > 0) {
         // C(-1): QK(0), loads of V(0) and K(1) (K(1) lands in an unused buffer if n == 1)
-        matrix_cluster(std::false_type{}, std::true_type{}, -1, pf, st, ids_v, ids_k);
+        matrix_cluster(std::false_type{}, std::true_type{}, -1, pf, st, ids_v, ids_k, std::false_type{});
         phase_end();
         for (int j = 0; j + 1 < n; ++j) {
             vector_cluster(j, st, pf);
             phase_end();
             // C(j): PV(j), QK(j+1), loads of V(j+1) and K(j+2) (the last K lands unused)
-            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k);
+            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k, std::true_type{});
             phase_end();
         }
         vector_cluster(n - 1, st, pf);
         phase_end();
         // The group's last tile may hold the sequence end: clear V past it.
         if ((tile_begin + n) * kTileKeys > total) pv(n - 1, pf, std::true_type{});
-        else matrix_cluster(std::true_type{}, std::false_type{}, n - 1, pf, st, ids_v, ids_k);
+        else matrix_cluster(std::true_type{}, std::false_type{}, n - 1, pf, st, ids_v, ids_k, std::false_type{});
         phase_end();
     }
     while (ph < phases) phase_end();
@@ -622,16 +660,23 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
         for (int b = 0; b < B; ++b) {
             const int64_t sb = (int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b];
             if (sb <= 0) continue;
-            wm.order[n] = b;
+            wm.seq[n] = b;
             tiles[b] = (int32_t)((sb * G + kRowsPerWG - 1) / kRowsPerWG);
             keys[b] = (int32_t)(host_prefix_lens[b] + sb);
             ++n;
         }
-        std::stable_sort(wm.order, wm.order + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
-        wm.cum[0] = 0;
-        for (int k = 0; k < n; ++k) wm.cum[k + 1] = wm.cum[k] + tiles[wm.order[k]];
+        std::stable_sort(wm.seq, wm.seq + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
+        int32_t cum = 0;
+        for (int k = 0; k < n; ++k) {
+            const int b = wm.seq[k];
+            cum += tiles[b];
+            wm.tiles_end[k] = cum;
+            wm.prefix[k] = host_prefix_lens[b];
+            wm.first[k] = host_cu_suffix[b];
+            wm.count[k] = host_cu_suffix[b + 1] - host_cu_suffix[b];
+        }
         wm.n_seq = n;
-        wm.per_head = wm.cum[n];
+        wm.per_head = cum;
         if (n == 0) return hipSuccess;
         n_items = (Hkv % kXcds == 0) ? (int64_t)wm.per_head * Hkv
                                      : ((int64_t)wm.per_head * Hkv + kXcds - 1) / kXcds * kXcds;
