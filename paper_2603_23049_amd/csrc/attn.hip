@@ -589,31 +589,35 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     while (ph < phases) phase_end();
 
     // ---- merge the two key halves through LDS, normalise, store ----
+    // Each group finalises half of the head dims (group 0 the first MT/2 blocks of 32,
+    // group 1 the rest): it sends the partner wave holding the same rows the other half
+    // of its accumulator and its (m, l), then merges the half it received.
     const float l_own = l_run[0] + l_run[1];
     const float l_tot = l_own + __shfl_xor(l_own, 32);
     const bool has_ref = thr > -INFINITY;      // this row saw a real score in this key half
+    constexpr int MH = MT / 2;
+    constexpr int XW = 4 * MH + 1;                 // float4 slots per lane: half of O, then (m, l)
+    static_assert(2 * kGroupWaves * XW * 64 * 16 <= (int)sizeof(lds), "merge area");
+    const int my0 = grp ? MH : 0, other0 = grp ? 0 : MH;
     __syncthreads();
-    float *xch = reinterpret_cast<float *>(&lds[0][0]);
-    constexpr int XW = 4 * MT + 1;                 // float4 slots per lane: O, then (m, l)
-    if (grp == 1) {
-        f32x4 *x4 = reinterpret_cast<f32x4 *>(xch) + (size_t)wg * XW * 64;
+    f32x4 *xch = reinterpret_cast<f32x4 *>(&lds[0][0]);
+    {
+        f32x4 *xo = xch + (size_t)(grp * kGroupWaves + wg) * XW * 64;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int k = 0; k < MH; ++k)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
                 f32x4 v;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) v[c] = o_acc[mt][4 * r4 + c];
-                x4[(mt * 4 + r4) * 64 + lane] = v;
+                for (int c = 0; c < 4; ++c) v[c] = o_acc[other0 + k][4 * r4 + c];
+                xo[(k * 4 + r4) * 64 + lane] = v;
             }
-        f32x4 ml = {has_ref ? m_ref : -INFINITY, l_tot, 0.f, 0.f};
-        x4[(XW - 1) * 64 + lane] = ml;
+        xo[(XW - 1) * 64 + lane] = f32x4{has_ref ? m_ref : -INFINITY, l_tot, 0.f, 0.f};
     }
     __syncthreads();
-    if (grp == 1) return;
 
-    const f32x4 *x4 = reinterpret_cast<const f32x4 *>(xch) + (size_t)wg * XW * 64;
-    const f32x4 ml = x4[(XW - 1) * 64 + lane];
+    const f32x4 *xi = xch + (size_t)((1 - grp) * kGroupWaves + wg) * XW * 64;
+    const f32x4 ml = xi[(XW - 1) * 64 + lane];
     const float m1 = ml[0], l1 = ml[1];
     const float m0 = has_ref ? m_ref : -INFINITY;
     const float mm = fmaxf(m0, m1);
@@ -623,15 +627,15 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     if (row_valid && tq < T) {
         u16 *orow = out + (tq * Hq + h) * D;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int k = 0; k < MH; ++k)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
-                const f32x4 o1 = x4[(mt * 4 + r4) * 64 + lane];
+                const f32x4 o1 = xi[(k * 4 + r4) * 64 + lane];
                 f32x4 v;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) v[c] = (a0 * o_acc[mt][4 * r4 + c] + a1 * o1[c]) * inv;
+                for (int c = 0; c < 4; ++c) v[c] = (a0 * o_acc[my0 + k][4 * r4 + c] + a1 * o1[c]) * inv;
                 const bf16x4 bv = __builtin_convertvector(v, bf16x4);
-                const int d0 = 32 * mt + 8 * r4 + 4 * half;
+                const int d0 = 32 * (my0 + k) + 8 * r4 + 4 * half;
                 *reinterpret_cast<u32x2 *>(orow + d0) = __builtin_bit_cast(u32x2, bv);
             }
     }
