@@ -20,6 +20,13 @@ Reported beside it:
   pipeline      the 32-layer two-stream pipeline: exposed load per layer,
                 the flow-shop least exposure, and their difference;
   cpu_baseline  the fp64 oracle on a bounded sample of the same layer.
+
+The copy, compute and offload streams of a pipeline overlap only if HIP maps them
+to different hardware queues. HIP maps a process's streams, in creation order,
+onto GPU_MAX_HW_QUEUES hardware queues (4 unless set), so with the several streams
+this script creates two of a pipeline's streams can share a queue and run in
+series; the script therefore raises the count to 8 (before HIP starts) unless the
+environment already sets it.
 """
 from __future__ import annotations
 
@@ -29,6 +36,8 @@ import math
 import os
 import sys
 import time
+
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
 
 import numpy as np
 

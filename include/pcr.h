@@ -289,6 +289,12 @@ typedef struct pcr_batch {
  * (append + attention), [4l+2] compute-stream wait before the layer (exposed
  * load), [4l+3] end of the layer's compute relative to the pipeline start; then
  * [4n] the whole pipeline ms and [4n+1] the sum of compute ms.
+ * Overlap needs copy_stream and compute_stream on different hardware queues:
+ * HIP maps a process's streams, in creation order, onto GPU_MAX_HW_QUEUES
+ * hardware queues (4 unless the environment sets it), and two streams on one
+ * queue run in series. Create these streams before others, or raise
+ * GPU_MAX_HW_QUEUES before HIP starts (the same holds for the three streams of
+ * pcr_pipeline_run_offload).
  */
 pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
                             pcr_load_method method, void *copy_stream, void *compute_stream,

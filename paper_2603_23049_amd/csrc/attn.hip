@@ -61,7 +61,7 @@ constexpr int kTileBlocks = kTileKeys / kBlockSize;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleThreshold = 8.0f;                // log2 units
 #ifndef KAHEAD
-#define KAHEAD 8
+#define KAHEAD 6
 #endif
 constexpr int kXcds = 8;                                 // MI355X: 8 XCDs, workgroups dealt round-robin
 
@@ -573,10 +573,24 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         // C(-1): QK(0), loads of V(0) and K(1) (K(1) lands in an unused buffer if n == 1)
         matrix_cluster(std::false_type{}, std::true_type{}, -1, pf, st, ids_v, ids_k, std::false_type{});
         phase_end();
-        for (int j = 0; j + 1 < n; ++j) {
+        // Two (M, C) pairs per iteration: the scores made in the first pair's matrix
+        // cluster feed the second pair's softmax in the same registers, which halves
+        // the register copies the loop-carried scores cost at the iteration boundary.
+        // C(j): PV(j), QK(j+1), loads of V(j+1) and K(j+2) (the last K lands unused).
+        int j = 0;
+        for (; j + 2 < n; j += 2) {
             vector_cluster(j, st, pf);
             phase_end();
-            // C(j): PV(j), QK(j+1), loads of V(j+1) and K(j+2) (the last K lands unused)
+            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k, std::true_type{});
+            phase_end();
+            vector_cluster(j + 1, st, pf);
+            phase_end();
+            matrix_cluster(std::true_type{}, std::true_type{}, j + 1, pf, st, ids_v, ids_k, std::true_type{});
+            phase_end();
+        }
+        if (j + 1 < n) {
+            vector_cluster(j, st, pf);
+            phase_end();
             matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k, std::true_type{});
             phase_end();
         }
