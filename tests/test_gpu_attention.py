@@ -78,6 +78,26 @@ def test_edge_shapes(d, G):
     _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"edges d={d} G={G}")
 
 
+@pytest.mark.parametrize("B", [100, 140])
+def test_many_sequences(B):
+    """More sequences than one lane of the work-map lookup holds (slots 64.. are read by
+    the second half of each lane's loads) and, at B = 140, more than the map holds
+    (plain order, lengths from the device arrays). Some sequences have no new tokens."""
+    rng = np.random.Generator(np.random.PCG64(1000 + B))
+    pl = [int(rng.integers(0, 80)) for _ in range(B)]
+    sl = [int(rng.integers(0, 24)) for _ in range(B)]
+    sl[0], sl[-1] = 0, 40
+    Hkv = 8
+    nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl)) + 7
+    b = synth.ragged_batch(f"many{B}", Hq=2 * Hkv, Hkv=Hkv, d=128, prefix_lens=pl, suffix_lens=sl,
+                           pool_blocks=nblocks, seed=20 + B)
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention many sequences B={b.B} T={b.T}")
+    L = _run(b, data, pk0, pv0)
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"B={B}")
+
+
 def test_l8b_layer_full_and_deterministic():
     b = synth.l8b_layer()
     data = synth.make_layer(b)
