@@ -300,9 +300,11 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
 
 
 def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
-    """One decode step (one new token per sequence, attending over ctx cached keys) of a
-    Llama-3-8B-shaped batch, attention only; pool, Q and tables drawn on the device (the
-    values do not change the work). HBM bytes = every key's K and V once + Q + out."""
+    """One decode step (one new token per sequence, attending over ctx keys) of a
+    Llama-3-8B-shaped batch, attention only, through the split-key decode entry point;
+    the prefill kernel on the same rows (one-token suffixes) is timed beside it. Pool, Q
+    and tables drawn on the device (the values do not change the work). HBM bytes =
+    every key's K and V once + Q + out."""
     import torch
     from paper_2603_23049_amd import pcr
     bs = 16
@@ -315,22 +317,33 @@ def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
     bt = torch.randperm(pool_blocks, device="cuda", generator=g).to(torch.int32).view(B, nb)
     q = torch.randn((B, Hq, d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
     out = torch.empty_like(q)
-    pl_h = np.full(B, ctx - 1, np.int32)
+    n_h = np.full(B, ctx, np.int32)
+    n_d = torch.from_numpy(n_h).cuda()
+    ws_bytes = pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, ctx)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+    pl_h = n_h - 1
     cu_h = np.arange(B + 1, dtype=np.int32)
     pl, cu = torch.from_numpy(pl_h).cuda(), torch.from_numpy(cu_h).cuda()
     s = torch.cuda.current_stream()
-    for _ in range(3):
-        pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)
-    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(s)
-    for _ in range(steps):
-        pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)
-    e.record(s)
-    e.synchronize()
-    ms = a.elapsed_time(e) / steps
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(steps):
+            fn()
+        e.record(s)
+        e.synchronize()
+        return a.elapsed_time(e) / steps
+
+    ms = timed(lambda: pcr.decode_attn(q, pool, bt, n_d, n_h, Hq, out, workspace=ws, stream=s))
+    ms_prefill = timed(lambda: pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s))
     nbytes = B * ctx * Hkv * d * 2 * 2 + 2 * B * Hq * d * 2
     return {"workload": f"decode B={B} ctx={ctx} Hq={Hq} Hkv={Hkv} d={d}", "attn_ms": ms, "hbm_bytes": nbytes,
-            "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3}
+            "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3,
+            "workspace_bytes": ws_bytes, "prefill_kernel_ms": ms_prefill,
+            "prefill_kernel_frac_hbm": nbytes / ms_prefill / 1e6 / HBM_PEAK_GBS}
 
 
 def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_chunks=96, request_compute_ms=30.0, n_serve=40):

@@ -239,6 +239,47 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
                                    void *stream);
 
 /*
+ * pcr_decode_attn -- one decode step: attention of one new query token per
+ * sequence over every key of that sequence (Sec. 2.2 with a one-token suffix:
+ * the output equals the last row of a full prefill of the sequence).
+ * For sequence b, query head h and keys j in [0, n_b):
+ *     out = sum_j softmax_j(sm_scale * <q, k_j>) v_j
+ * where n_b = context_lens[b] counts the cached tokens plus the token being
+ * decoded, whose K/V must already be in the pool (pcr_append_kv).
+ *   q                  device bf16 [B][Hq][d], 16-byte aligned
+ *   block_tables       device int32 [B][max_blocks]; entries past ceil(n_b/bs) are not read
+ *   context_lens       device int32 [B]; host_context_lens: host copy of the same
+ *                      (sizes the launch; the two must be equal)
+ *   out                device bf16 [B][Hq][d], 16-byte aligned; fp32 accumulation,
+ *                      rounded to nearest even
+ *   workspace          device memory owned by the caller, 16-byte aligned, of at least
+ *                      pcr_decode_attn_workspace_size(B, Hq, Hkv, d, max_b n_b) bytes
+ *                      (NULL when that is 0); its contents are scratch. One workspace
+ *                      serves every call ordered on one stream; calls that may overlap
+ *                      need their own.
+ * The key range of each (sequence, kv head) is split into chunks processed in
+ * parallel and merged exactly (a second kernel on the same stream), so the
+ * result does not depend on the split beyond fp32 rounding.
+ * Errors: PCR_ERR_UNSUPPORTED if Hq/Hkv > 16 (pcr_prefix_prefill_attn with
+ * one-token suffixes covers that case); PCR_ERR_INVALID_ARG if some n_b < 1,
+ * ceil(n_b/bs) > max_blocks, or the workspace is missing or too small (the
+ * message names the size needed). B = 0 is a no-op.
+ */
+pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                           int32_t max_blocks, const int32_t *context_lens, const int32_t *host_context_lens,
+                           int32_t B, int32_t num_q_heads, float sm_scale, void *out, void *workspace,
+                           int64_t workspace_bytes, void *stream);
+
+/*
+ * pcr_decode_attn_workspace_size -- bytes of workspace pcr_decode_attn needs on the
+ * current device for any batch of B sequences whose context lengths are at most
+ * max_context (0 when every such batch is handled without one). Queries the
+ * device's compute-unit count; PCR_ERR_HIP when no device is usable.
+ */
+pcr_status pcr_decode_attn_workspace_size(int32_t B, int32_t num_q_heads, int32_t num_kv_heads,
+                                          int32_t head_dim, int32_t max_context, int64_t *bytes);
+
+/*
  * pcr_gather_kv -- read tokens back out of the pool in logical order (the
  * staging step of a layer-wise offload, Sec. 4.3; also a test aid).
  * For each sequence b, tokens starts[b] .. starts[b]+lens[b]-1 go to rows

@@ -1,0 +1,359 @@
+// Split-key decode attention for gfx950: one query token per sequence (bf16 in,
+// fp32 accumulate, bf16 out).
+//
+// For sequence b with n_b visible keys (its cached context plus the token being
+// decoded) and query head h: out = softmax_j(sm_scale <q, k_j>) v_j over
+// j = 0 .. n_b - 1, K/V read from the paged pool through the block table. This
+// is the suffix row of a sequence with prefix n_b - 1 and a one-token suffix
+// (Sec. 2.2); the prefill kernel computes the same rows inside mixed batches,
+// but its 128-row tiles would carry only G = Hq/Hkv useful rows here, and a
+// decode step is bound by reading K/V from HBM, not by matrix work.
+//
+// Work decomposition. The key range of each (sequence, kv head) is cut into
+// n_split chunks of `chunk` keys (a multiple of 32). Each chunk is the task of
+// one wave; the host picks n_split so that every SIMD gets about one wave. A wave holds the G query heads of its kv head as the columns of
+// v_mfma_f32_16x16x32_bf16 tiles (G <= 16) and walks its chunk 32 keys (two
+// pool blocks) at a time:
+//   S^T[key][h] = K Q^T     A = 16 key rows x 32 dims of K,  B = Q^T (registers)
+//   O^T[d][h]  += V^T P^T   A = 16 dims x 32 keys of V^T,    B = P^T (registers)
+// No operand is shared between waves, so K and V go from HBM straight into
+// registers: K is key-major and V d-major inside each pool block, so every A
+// operand is one 16-byte run. Two register sets alternate: the loads of the
+// next 32 keys are in flight while the current ones are used. Lane (c, q4)
+// (c = lane % 16, q4 = lane / 16) loads key row 8*(c/4) + 4r + c%4 for the r-th
+// K product, so that its eight scores are keys 8*q4 .. 8*q4 + 7 of the step,
+// which are exactly its eight P^T operand values in the V product: the
+// softmax is in-lane apart from the column max over the four lanes of a column.
+//
+// K/V loads are non-temporal: every byte is used once, and streaming them past
+// the caches measured about 10% faster than ordinary loads.
+//
+// A chunk that covers its whole sequence writes the output row. Up to four
+// chunks of one (sequence, kv head) form one workgroup and are merged through
+// LDS (running max and sum in the log2 domain). With more chunks, each wave
+// writes its unnormalised O, max and sum to the workspace and
+// decode_combine_kernel merges the chunks of each (sequence, head).
+#include <algorithm>
+
+#include "pcr_internal.h"
+
+namespace pcr {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16;
+
+constexpr int kWaves = 4;              // tasks (waves) per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kStepKeys = 32;          // keys per step: two pool blocks
+constexpr int kMaxCols = 16;           // query heads per kv head held by one tile
+// Waves per CU the split count aims at. The kernel's registers allow two per SIMD
+// (four for d = 64), but one wave per SIMD, each with two steps of loads in flight,
+// streams K/V from HBM faster than two.
+constexpr int waves_per_cu(int) { return 4; }
+constexpr int kMinChunk = 256;         // keys; shorter chunks spend more on set-up than on loads
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <int D>
+struct StepRegs {
+    u32x4 k[2][D / 32];   // K operands of the two products (row group r, dims 32*kk ..)
+    u32x4 v[D / 16];      // V^T operands (dims 16*mt ..)
+};
+
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_split_kernel(
+    const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
+    int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
+    const int32_t *__restrict__ context_lens, int32_t B, int32_t Hq, int32_t n_split, int32_t chunk,
+    float scale_log2, int32_t lds_merge, u16 *__restrict__ out, float *__restrict__ ws_o,
+    float *__restrict__ ws_ml)
+{
+    constexpr int KK = D / 32;    // K products per row group (32 dims each)
+    constexpr int MT = D / 16;    // V products (16 dims each)
+    const int lane = (int)(threadIdx.x & 63);
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int wg_waves = (int)(blockDim.x >> 6);   // n_split when the chunks merge in LDS
+    const int64_t task = (int64_t)blockIdx.x * wg_waves + wave;
+    if (task >= (int64_t)B * Hkv * n_split) return;   // never for a merging workgroup (exact grid)
+    const int sp = (int)(task % n_split);
+    const int bg = (int)(task / n_split);
+    const int g = bg % Hkv, b = bg / Hkv;
+    const int n_keys = context_lens[b];
+    const int kbeg = sp * chunk;
+    const bool active = kbeg < n_keys;             // wave-uniform
+    if (!active && !lds_merge) return;             // a merging wave stays for the barrier
+    const int kend = min(n_keys, kbeg + chunk);
+    const int last_blk = min((n_keys - 1) >> 4, max_blocks - 1);   // last logical block with a visible key
+    const int G = Hq / Hkv;
+    const int c = lane & 15, q4 = lane >> 4;
+    const bool col = c < G;
+    const int h = g * G + c;
+
+    // Q^T operands: lane (c, q4) holds dims 32*kk + 8*q4 .. +7 of head h (zero past G).
+    u32x4 qf[KK];
+    {
+        const u16 *qrow = q + ((int64_t)b * Hq + (col ? h : g * G)) * D + 8 * q4;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const u32x4 raw = *reinterpret_cast<const u32x4 *>(qrow + 32 * kk);
+            qf[kk] = col ? raw : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+
+    const int32_t *bt_row = block_tables + (int64_t)b * max_blocks;
+    auto block_id = [&](int li) -> int32_t {
+        const int32_t id = bt_row[min(li, last_blk)];
+        return (uint32_t)id < (uint32_t)num_blocks ? id : 0;   // a bad entry reads block 0, never outside
+    };
+    const int krow = 8 * ((c >> 2) & 1) + (c & 3);    // slot of row group 0; row group 1 is 4 slots on
+    auto load_step = [&](int step, StepRegs<D> &R) {
+        const int li = (kbeg + step * kStepKeys) >> 4;
+        const int32_t b0 = block_id(li), b1 = block_id(li + 1);
+        const int32_t kb = (c >> 3) ? b1 : b0;
+        const int32_t vb = (q4 >> 1) ? b1 : b0;
+        const u16 *kp = pool_k + ((int64_t)kb * Hkv + g) * (kBlockSize * D) + krow * D + 8 * q4;
+        const u16 *vp = pool_v + ((int64_t)vb * Hkv + g) * (kBlockSize * D) + c * kBlockSize + 8 * (q4 & 1);
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                R.k[r][kk] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(kp + 4 * r * D + 32 * kk));
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            R.v[mt] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(vp + 16 * mt * kBlockSize));
+    };
+
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4 o[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto process = [&](int step, const StepRegs<D> &R) {
+        f32x4 s[2];
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            s[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                s[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(R.k[r][kk]), as_bf16x8(qf[kk]), s[r],
+                                                               0, 0, 0);
+        }
+        const int k0 = kbeg + step * kStepKeys;
+        if (k0 + kStepKeys > kend) {               // wave-uniform: only a chunk's last step is ragged
+#pragma unroll
+            for (int r = 0; r < 2; ++r)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (k0 + 8 * q4 + 4 * r + i >= kend) s[r][i] = -INFINITY;
+        }
+        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx * scale_log2);   // finite: key k0 is visible
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        bf16x8 pb;
+        float ps = 0.f;
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r][i], scale_log2, -m_new));
+                pb[4 * r + i] = (__bf16)p;
+                ps += p;
+            }
+        l_run = l_run * alpha + ps;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {   // the max rose in some column
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            o[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(R.v[mt]), pb, o[mt], 0, 0, 0);
+    };
+
+    // Register set ra always holds the loads of step j when an iteration starts, so
+    // every load inside the loop is unconditional and the wait before each step
+    // leaves the other set's 16 loads in flight.
+    if (active) {
+        const int n_steps = (kend - kbeg + kStepKeys - 1) / kStepKeys;
+        StepRegs<D> ra, rb;
+        load_step(0, ra);
+        int j = 0;
+        for (; j + 2 < n_steps; j += 2) {
+            load_step(j + 1, rb);
+            process(j, ra);
+            load_step(j + 2, ra);
+            process(j + 1, rb);
+        }
+        if (j + 1 < n_steps) {
+            load_step(j + 1, rb);
+            process(j, ra);
+            process(j + 1, rb);
+        } else {
+            process(j, ra);
+        }
+    }
+
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (lds_merge) {
+        // The workgroup holds every chunk of one (sequence, kv head). Waves 1.. leave
+        // their O (lane layout), max and sum in LDS; wave 0 merges and writes. A chunk
+        // past the sequence's end contributes max -inf, sum 0, O 0; chunk 0 always has
+        // keys, so the merged max is finite.
+        extern __shared__ f32x4 part_o[];          // [wave][MT][64 lanes]
+        f32x2 *part_ml = reinterpret_cast<f32x2 *>(part_o + wg_waves * MT * 64);   // [wave][64 lanes]
+        if (wave > 0) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) part_o[(wave * MT + mt) * 64 + lane] = o[mt];
+            part_ml[wave * 64 + lane] = f32x2{m_run, l_tot};
+        }
+        __syncthreads();
+        if (wave > 0) return;
+        float M = m_run;
+        for (int w = 1; w < wg_waves; ++w) M = fmaxf(M, part_ml[w * 64 + lane][0]);
+        const float a0 = __builtin_amdgcn_exp2f(m_run - M);
+        l_tot *= a0;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) o[mt] *= a0;
+        for (int w = 1; w < wg_waves; ++w) {
+            const f32x2 ml = part_ml[w * 64 + lane];
+            const float a = __builtin_amdgcn_exp2f(ml[0] - M);
+            l_tot += a * ml[1];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) o[mt] += a * part_o[(w * MT + mt) * 64 + lane];
+        }
+    }
+    if (!col) return;
+    if (lds_merge || (kbeg == 0 && kend == n_keys)) {   // merged, or the only chunk of its sequence
+        const float inv = 1.f / l_tot;
+        u16 *orow = out + ((int64_t)b * Hq + h) * D + 4 * q4;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const bf16x4 v = __builtin_convertvector(o[mt] * inv, bf16x4);
+            *reinterpret_cast<u32x2 *>(orow + 16 * mt) = __builtin_bit_cast(u32x2, v);
+        }
+        return;
+    }
+    const int64_t part = task * G + c;
+    float *po = ws_o + part * D + 4 * q4;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<f32x4 *>(po + 16 * mt) = o[mt];
+    if (q4 == 0) *reinterpret_cast<f32x2 *>(ws_ml + 2 * part) = f32x2{m_run, l_tot};
+}
+
+// One wave per (sequence, query head) of a sequence cut into more than one chunk:
+// out = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c with M = max_c m_c.
+template <int D>
+__global__ __launch_bounds__(kThreads) void decode_combine_kernel(
+    const float *__restrict__ ws_o, const float *__restrict__ ws_ml, const int32_t *__restrict__ context_lens,
+    int32_t B, int32_t Hkv, int32_t Hq, int32_t n_split, int32_t chunk, u16 *__restrict__ out)
+{
+    constexpr int E = D / 64;     // output elements per lane
+    const int lane = (int)(threadIdx.x & 63);
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int64_t pair = (int64_t)blockIdx.x * kWaves + wave;
+    if (pair >= (int64_t)B * Hq) return;
+    const int h = (int)(pair % Hq), b = (int)(pair / Hq);
+    const int G = Hq / Hkv, g = h / G, c = h % G;
+    const int n_keys = context_lens[b];
+    const int ns = min((n_keys + chunk - 1) / chunk, n_split);
+    if (ns <= 1) return;                            // written by the split kernel
+    const int64_t part0 = ((int64_t)b * Hkv + g) * n_split * G + c;
+    float M = -INFINITY;
+    for (int k = 0; k < ns; ++k) M = fmaxf(M, ws_ml[2 * (part0 + (int64_t)k * G)]);
+    float L = 0.f, acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    for (int k = 0; k < ns; ++k) {
+        const int64_t part = part0 + (int64_t)k * G;
+        const f32x2 ml = *reinterpret_cast<const f32x2 *>(ws_ml + 2 * part);
+        const float w = __builtin_amdgcn_exp2f(ml[0] - M);
+        L += w * ml[1];
+        const float *po = ws_o + part * D + E * lane;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] += w * po[e];
+    }
+    const float inv = 1.f / L;
+    u16 *orow = out + ((int64_t)b * Hq + h) * D + E * lane;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const __bf16 v = (__bf16)(acc[e] * inv);
+        orow[e] = __builtin_bit_cast(u16, v);
+    }
+}
+
+}  // namespace
+
+DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t max_context, int32_t n_cu)
+{
+    DecodePlan p{};
+    const int64_t pairs = (int64_t)B * num_kv_heads;
+    if (pairs <= 0 || max_context <= 0) return p;
+    const int64_t want = ((int64_t)n_cu * waves_per_cu(head_dim) + pairs - 1) / pairs;
+    const int64_t cap = ((int64_t)max_context + kMinChunk - 1) / kMinChunk;
+    const int64_t bound = std::max<int64_t>(1, std::min(want, cap));
+    int64_t chunk = ((int64_t)max_context + bound - 1) / bound;
+    chunk = (chunk + kStepKeys - 1) / kStepKeys * kStepKeys;
+    const int64_t G = num_q_heads / num_kv_heads;
+    p.bound_split = (int32_t)bound;
+    p.chunk = (int32_t)chunk;
+    p.n_split = (int32_t)(((int64_t)max_context + chunk - 1) / chunk);
+    p.workspace_bytes = p.n_split > kWaves ? pairs * p.n_split * G * (head_dim + 2) * 4 : 0;
+    p.bound_workspace_bytes = bound > kWaves ? pairs * bound * G * (head_dim + 2) * 4 : 0;
+    return p;
+}
+
+int decode_max_cols() { return kMaxCols; }
+
+hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int32_t *block_tables,
+                              int32_t max_blocks, const int32_t *context_lens, int32_t B, int32_t num_q_heads,
+                              const DecodePlan &plan, float sm_scale, void *out, void *workspace, hipStream_t s)
+{
+    const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv, D = pool.head_dim;
+    const int64_t n_tasks = (int64_t)B * Hkv * plan.n_split;
+    // Up to kWaves chunks of a sequence share one workgroup and merge in LDS; more go
+    // through the workspace and decode_combine_kernel.
+    const bool through_ws = plan.n_split > kWaves;
+    const int lds_merge = plan.n_split > 1 && !through_ws;
+    const int wg_waves = through_ws ? kWaves : plan.n_split;
+    const dim3 grid((unsigned)((n_tasks + wg_waves - 1) / wg_waves));
+    const size_t lds = lds_merge ? (size_t)wg_waves * 64 * ((D / 16) * 16 + 8) : 0;
+    float *ws_o = through_ws ? static_cast<float *>(workspace) : nullptr;
+    float *ws_ml = through_ws ? ws_o + n_tasks * G * D : nullptr;
+    const float scale_log2 = sm_scale * kLog2e;
+    auto *qq = static_cast<const u16 *>(q);
+    auto *pk = static_cast<const u16 *>(pool.k);
+    auto *pv = static_cast<const u16 *>(pool.v);
+    auto *oo = static_cast<u16 *>(out);
+    if (D == 128)
+        hipLaunchKernelGGL(decode_split_kernel<128>, grid, dim3(64 * wg_waves), lds, s, qq, pk, pv, pool.num_blocks,
+                           Hkv, block_tables, max_blocks, context_lens, B, num_q_heads, plan.n_split, plan.chunk,
+                           scale_log2, lds_merge, oo, ws_o, ws_ml);
+    else
+        hipLaunchKernelGGL(decode_split_kernel<64>, grid, dim3(64 * wg_waves), lds, s, qq, pk, pv, pool.num_blocks,
+                           Hkv, block_tables, max_blocks, context_lens, B, num_q_heads, plan.n_split, plan.chunk,
+                           scale_log2, lds_merge, oo, ws_o, ws_ml);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !through_ws) return e;
+    const dim3 cgrid((unsigned)(((int64_t)B * num_q_heads + kWaves - 1) / kWaves));
+    if (D == 128)
+        hipLaunchKernelGGL(decode_combine_kernel<128>, cgrid, dim3(kThreads), 0, s, ws_o, ws_ml, context_lens, B,
+                           Hkv, num_q_heads, plan.n_split, plan.chunk, oo);
+    else
+        hipLaunchKernelGGL(decode_combine_kernel<64>, cgrid, dim3(kThreads), 0, s, ws_o, ws_ml, context_lens, B,
+                           Hkv, num_q_heads, plan.n_split, plan.chunk, oo);
+    return hipGetLastError();
+}
+
+}  // namespace pcr

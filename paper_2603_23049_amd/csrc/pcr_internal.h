@@ -49,6 +49,24 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s);
 
+// Decode attention (decode.hip). The key range of each (sequence, kv head) is cut
+// into n_split chunks of `chunk` keys; bound_split is the split count for the
+// largest context the plan was made for, an upper bound of n_split for every
+// smaller one (the workspace sizes follow the two counts).
+struct DecodePlan {
+    int32_t n_split;
+    int32_t chunk;
+    int32_t bound_split;
+    int64_t workspace_bytes;
+    int64_t bound_workspace_bytes;
+};
+DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t max_context, int32_t n_cu);
+int decode_max_cols();
+hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int32_t *block_tables,
+                              int32_t max_blocks, const int32_t *context_lens, int32_t B, int32_t num_q_heads,
+                              const DecodePlan &plan, float sm_scale, void *out, void *workspace, hipStream_t s);
+
 // Pool-to-host offload with any method (the staged one takes the workspace); used by
 // the pipeline, which chooses the method per call.
 pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,

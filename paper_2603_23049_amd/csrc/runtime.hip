@@ -631,6 +631,96 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const
     return PCR_OK;
 }
 
+static pcr_status decode_heads_ok(int32_t num_q_heads, int32_t num_kv_heads, const char *who)
+{
+    if (num_q_heads <= 0 || num_q_heads % num_kv_heads != 0)
+        return fail(PCR_ERR_UNSUPPORTED, "%s: num_q_heads %d is not a positive multiple of num_kv_heads %d", who,
+                    num_q_heads, num_kv_heads);
+    if (num_q_heads / num_kv_heads > decode_max_cols())
+        return fail(PCR_ERR_UNSUPPORTED, "%s: more than %d query heads per kv head (use pcr_prefix_prefill_attn "
+                    "with one-token suffixes)", who, decode_max_cols());
+    return PCR_OK;
+}
+
+static pcr_status device_cu_count(int32_t *n_cu, const char *who)
+{
+    int dev = 0, cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    *n_cu = cu > 0 ? cu : 1;
+    return PCR_OK;
+}
+
+pcr_status pcr_decode_attn_workspace_size(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                          int32_t max_context, int64_t *bytes)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_decode_attn_workspace_size";
+    if (!bytes) return fail(PCR_ERR_INVALID_ARG, "%s: bytes is NULL", who);
+    *bytes = 0;
+    pcr_status st = check_layout(kBlockSize, num_kv_heads, head_dim, who);
+    if (st) return st;
+    st = decode_heads_ok(num_q_heads, num_kv_heads, who);
+    if (st) return st;
+    if (B < 0 || max_context < 0) return fail(PCR_ERR_INVALID_ARG, "%s: negative B or max_context", who);
+    if (B == 0 || max_context == 0) return PCR_OK;
+    int32_t n_cu = 0;
+    st = device_cu_count(&n_cu, who);
+    if (st) return st;
+    *bytes = decode_plan(B, num_q_heads, num_kv_heads, head_dim, max_context, n_cu).bound_workspace_bytes;
+    return PCR_OK;
+}
+
+pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
+                           const int32_t *context_lens, const int32_t *host_context_lens, int32_t B,
+                           int32_t num_q_heads, float sm_scale, void *out, void *workspace, int64_t workspace_bytes,
+                           void *stream)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_decode_attn";
+    pcr_status st = check_pool(pool, who);
+    if (st) return st;
+    if (B < 0) return fail(PCR_ERR_INVALID_ARG, "%s: B < 0", who);
+    if (B == 0) return PCR_OK;
+    if (!host_context_lens) return fail(PCR_ERR_INVALID_ARG, "%s: NULL host length array", who);
+    st = decode_heads_ok(num_q_heads, pool->num_kv_heads, who);
+    if (st) return st;
+    if (!(sm_scale > 0.f) || !(sm_scale < 1e30f)) return fail(PCR_ERR_INVALID_ARG, "%s: bad sm_scale", who);
+    if (max_blocks <= 0) return fail(PCR_ERR_INVALID_ARG, "%s: max_blocks must be positive", who);
+    if ((int64_t)B * num_q_heads > (int64_t)1 << 30)
+        return fail(PCR_ERR_UNSUPPORTED, "%s: batch too large for one launch", who);
+    int32_t max_ctx = 0;
+    for (int b = 0; b < B; ++b) {
+        const int32_t n = host_context_lens[b];
+        if (n < 1) return fail(PCR_ERR_INVALID_ARG, "%s: sequence %d has no visible key", who, b);
+        if (ceil_div(n, kBlockSize) > max_blocks)
+            return fail(PCR_ERR_INVALID_ARG, "%s: sequence %d needs more blocks than max_blocks %d", who, b,
+                        max_blocks);
+        max_ctx = std::max(max_ctx, n);
+    }
+    if (!q || !out || !block_tables || !context_lens)
+        return fail(PCR_ERR_INVALID_ARG, "%s: NULL device argument", who);
+    if (((uintptr_t)q | (uintptr_t)out) & 15)
+        return fail(PCR_ERR_INVALID_ARG, "%s: q/out must be 16-byte aligned", who);
+    int32_t n_cu = 0;
+    st = device_cu_count(&n_cu, who);
+    if (st) return st;
+    const DecodePlan plan = decode_plan(B, num_q_heads, pool->num_kv_heads, pool->head_dim, max_ctx, n_cu);
+    if (plan.workspace_bytes > 0) {
+        if (!workspace || workspace_bytes < plan.workspace_bytes)
+            return fail(PCR_ERR_INVALID_ARG, "%s: this batch needs a workspace of %lld bytes (%lld given)", who,
+                        (long long)plan.workspace_bytes, (long long)(workspace ? workspace_bytes : 0));
+        if ((uintptr_t)workspace & 15)
+            return fail(PCR_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+    }
+    hipError_t e = launch_decode_attn(q, *pool, block_tables, max_blocks, context_lens, B, num_q_heads, plan,
+                                      sm_scale, out, workspace, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "pcr_decode_attn: launch");
+    return PCR_OK;
+}
+
 pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
                          const int32_t *starts, const int32_t *cu_out, int32_t B, int32_t total, void *k_out,
                          void *v_out, void *stream)

@@ -33,7 +33,7 @@ LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block":
 EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_layer_method",
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
-           "pcr_prefix_prefill_attn", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
+           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
            "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
            "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
 
@@ -87,6 +87,9 @@ def lib():
         L.pcr_append_kv.argtypes = [ctypes.POINTER(_Pool), P, P, P, i32, P]
         L.pcr_prefix_prefill_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, P, P, i32, i32,
                                               ctypes.c_float, P, P]
+        L.pcr_decode_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, ctypes.c_float, P, P,
+                                      i64, P]
+        L.pcr_decode_attn_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int64)]
         L.pcr_gather_kv.argtypes = [ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, P, P, P]
         L.pcr_pipeline_run.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), ctypes.c_int, P, P,
                                        P]
@@ -291,6 +294,35 @@ def prefix_prefill_attn(q, pool: KVPool, block_tables, prefix_lens, cu_suffix, h
     _check(lib().pcr_prefix_prefill_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
                                          _ptr(prefix_lens), _ptr(cu_suffix), _ptr(hpl), _ptr(hcu), B,
                                          int(num_q_heads), float(sm_scale), _ptr(out), _stream(stream)))
+
+
+def decode_attn_workspace_bytes(B: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                                max_context: int) -> int:
+    """pcr_decode_attn_workspace_size on the current device."""
+    n = ctypes.c_int64(0)
+    _check(lib().pcr_decode_attn_workspace_size(int(B), int(num_q_heads), int(num_kv_heads), int(head_dim),
+                                                int(max_context), ctypes.byref(n)))
+    return int(n.value)
+
+
+def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, num_q_heads: int, out,
+                workspace=None, sm_scale: Optional[float] = None, stream=None):
+    """pcr_decode_attn. q/out [B][Hq][d], block_tables [B][max_blocks], context_lens [B] on the
+    device; host_context_lens is the host copy. Without a workspace one of the needed size
+    is allocated on q's device."""
+    hcl = _i32_host(host_context_lens)
+    B = int(hcl.shape[0])
+    if sm_scale is None:
+        sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    if workspace is None and B > 0:
+        import torch
+        n = decode_attn_workspace_bytes(B, num_q_heads, pool.num_kv_heads, pool.head_dim, int(hcl.max()))
+        workspace = torch.empty(n, dtype=torch.uint8, device=q.device) if n > 0 else None
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    p = pool.c()
+    _check(lib().pcr_decode_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
+                                 _ptr(context_lens), _ptr(hcl), B, int(num_q_heads), float(sm_scale), _ptr(out),
+                                 _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def gather_kv(pool: KVPool, block_tables, starts, cu_out, total: int, k_out, v_out, stream=None):

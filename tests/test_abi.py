@@ -107,6 +107,27 @@ def test_argument_validation_before_any_device_work():
     hcu0 = np.array([0, 0], np.int32)
     assert L.pcr_prefix_prefill_attn(16, P(_pool()), 16, 4, 16, 16, hpl.ctypes.data, hcu0.ctypes.data, 1, 1,
                                      0.125, 16, None) == pcr.PCR_OK
+    # decode: more than 16 query heads per kv head, a sequence with no key, a too-short
+    # block table, bad scale; B = 0 is a no-op (all rejected before the device is asked
+    # for its compute-unit count)
+    hcl = np.array([40, 1], np.int32)
+    dargs = lambda Hq, scale, mb, lens: (16, P(_pool(Hkv=2)), 16, mb, 16, lens.ctypes.data, 2, Hq, scale, 16,
+                                         None, 0, None)
+    assert L.pcr_decode_attn(*dargs(34, 0.125, 4, hcl)) == pcr.PCR_ERR_UNSUPPORTED
+    assert "query heads per kv head" in pcr.last_error()
+    assert L.pcr_decode_attn(*dargs(3, 0.125, 4, hcl)) == pcr.PCR_ERR_UNSUPPORTED
+    assert L.pcr_decode_attn(*dargs(4, 0.0, 4, hcl)) == pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_decode_attn(*dargs(4, 0.125, 2, hcl)) == pcr.PCR_ERR_INVALID_ARG
+    assert "max_blocks" in pcr.last_error()
+    assert L.pcr_decode_attn(*dargs(4, 0.125, 4, np.array([40, 0], np.int32))) == pcr.PCR_ERR_INVALID_ARG
+    assert "no visible key" in pcr.last_error()
+    assert L.pcr_decode_attn(16, P(_pool()), 16, 4, 16, hcl.ctypes.data, 0, 1, 0.125, 16, None, 0, None) == \
+        pcr.PCR_OK
+    nbytes = ctypes.c_int64(-1)
+    assert L.pcr_decode_attn_workspace_size(4, 34, 2, 128, 100, ctypes.byref(nbytes)) == pcr.PCR_ERR_UNSUPPORTED
+    assert L.pcr_decode_attn_workspace_size(4, 8, 2, 96, 100, ctypes.byref(nbytes)) == pcr.PCR_ERR_UNSUPPORTED
+    assert L.pcr_decode_attn_workspace_size(0, 8, 2, 128, 100, ctypes.byref(nbytes)) == pcr.PCR_OK
+    assert nbytes.value == 0
     # load: block ids out of range and repeated destinations are caught on the host
     host = pcr._Host(0x30000, 0x40000, 8, 16, 1, 64)
     src = np.array([0, 9], np.int32)

@@ -1,6 +1,11 @@
 """GPU: decode rows (one new token per sequence) in the same attention launch as
-prefill rows, and a 16-step decode loop (append one token, attend over everything
-so far) against the fp64 oracle at every step."""
+prefill rows; the split-key decode entry point on ragged contexts, many short
+sequences, every supported head shape and the decode-step benchmark's full size;
+and a 16-step decode loop (append one token, attend over everything so far)
+through both attention entry points, against the fp64 oracle at every step.
+
+A decode row of a sequence with n visible keys is the oracle's suffix row of a
+sequence with prefix n - 1 and a one-token suffix."""
 import numpy as np
 import pytest
 import torch
@@ -19,6 +24,139 @@ def _check(got, want, label):
     mx, mean = error_stats(got, want)
     say(f"    {label}: max_abs={mx:.3e} mean_abs={mean:.3e}")
     assert np.all(np.isfinite(got)) and mx <= MAX_ABS and mean <= MEAN_ABS, (label, mx, mean)
+
+
+def _decode_oracle(q, pk, pv, bt, ctx, Hkv, rows=None):
+    pl = np.asarray(ctx, np.int32) - 1
+    cu = np.arange(len(ctx) + 1, dtype=np.int32)
+    return oattn.attention(q, pk, pv, bt, pl, cu, Hkv, BS, rows=rows)
+
+
+def _decode_inputs(ctx, Hq, Hkv, d, seed, pool_blocks=None):
+    """Random block tables (distinct blocks per sequence unless pool_blocks is given,
+    then drawn with repeats from that many blocks), padded with -1; bf16 N(0,1) pool
+    and queries."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    nbs = [-(-n // BS) for n in ctx]
+    bt = np.full((len(ctx), max(nbs) + 1), -1, np.int32)
+    if pool_blocks is None:
+        pool_blocks = sum(nbs) + 3
+        perm = rng.permutation(pool_blocks).astype(np.int32)
+        cum = np.concatenate([[0], np.cumsum(nbs)])
+        for i, nb in enumerate(nbs):
+            bt[i, :nb] = perm[cum[i]:cum[i] + nb]
+    else:
+        for i, nb in enumerate(nbs):
+            bt[i, :nb] = rng.integers(0, pool_blocks, nb, dtype=np.int32)
+    shape = (pool_blocks, Hkv, BS * d)
+    pk, pv = synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
+    q = synth.normal_bf16(rng, (len(ctx), Hq, d))
+    return q, pk, pv, bt
+
+
+def _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=None):
+    pool = pcr.KVPool(dev(pk), dev(pv), Hkv, d)
+    out = torch.zeros((len(ctx), Hq, d), dtype=torch.int16, device="cuda")
+    cl = np.asarray(ctx, np.int32)
+    pcr.decode_attn(dev(q), pool, dev(bt), dev(cl), cl, Hq, out, workspace=workspace)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("Hq,Hkv,d", [(32, 8, 128), (64, 8, 128), (64, 4, 128), (8, 8, 128), (32, 8, 64),
+                                      (16, 1, 64)])
+def test_decode_ragged_contexts(Hq, Hkv, d):
+    """Contexts of one key, within one block, at block, step and chunk boundaries, and
+    long: single-chunk sequences write the output directly, the others (cut into more
+    than four chunks at this batch size) go through the workspace and the merge kernel."""
+    ctx = [1, 2, 15, 16, 17, 31, 32, 33, 63, 255, 256, 257, 288, 289, 1000, 1088, 1089, 2176, 3001, 4352]
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=7 + Hq + d)
+    say(f"[gpu] decode ragged Hq={Hq} Hkv={Hkv} d={d} B={len(ctx)} "
+        f"workspace={pcr.decode_attn_workspace_bytes(len(ctx), Hq, Hkv, d, max(ctx))}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode Hq={Hq} Hkv={Hkv} d={d}")
+
+
+@pytest.mark.parametrize("B,d", [(32, 128), (48, 128), (100, 128), (32, 64)])
+def test_decode_ragged_merged_in_workgroup(B, d):
+    """Batches whose sequences are cut into 2-4 chunks merged inside one workgroup (no
+    workspace): ragged contexts, so some chunks lie past a short sequence's end."""
+    Hq, Hkv = 32, 8
+    rng = np.random.Generator(np.random.PCG64(B + d))
+    ctx = [int(x) for x in rng.integers(1, 4353, B)]
+    ctx[:6] = [1, 16, 33, 1100, 2200, 4352]
+    assert pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, max(ctx)) == 0
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=B * 3 + d)
+    say(f"[gpu] decode merged in workgroup B={B} d={d}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode merged B={B} d={d}")
+
+
+def test_decode_many_short_sequences_without_workspace():
+    """300 sequences of 1-300 keys: one chunk each, so no workspace is needed or passed."""
+    rng = np.random.Generator(np.random.PCG64(5))
+    ctx = [int(x) for x in rng.integers(1, 301, 300)]
+    ctx[0], ctx[1] = 1, 300
+    Hq, Hkv, d = 32, 8, 128
+    assert pcr.decode_attn_workspace_bytes(len(ctx), Hq, Hkv, d, max(ctx)) == 0
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=6)
+    say("[gpu] decode 300 short sequences")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=None)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), "decode short")
+
+
+def test_decode_workspace_checked():
+    """A workspace smaller than the batch needs is refused before anything is enqueued."""
+    ctx = [4000, 3000]
+    Hq, Hkv, d = 32, 8, 128
+    need = pcr.decode_attn_workspace_bytes(len(ctx), Hq, Hkv, d, max(ctx))
+    assert need > 0
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=8)
+    small = torch.empty(need // 2, dtype=torch.uint8, device="cuda")
+    with pytest.raises(pcr.PcrError) as e:
+        _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=small)
+    assert e.value.status == pcr.PCR_ERR_INVALID_ARG and "workspace" in str(e.value)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=ws)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), "decode exact workspace")
+
+
+def test_decode_step_full_size_sampled_and_deterministic():
+    """The decode-step benchmark's shape (64 sequences x 4352 keys, 32 q / 8 kv heads,
+    d = 128) in its launch configuration, over a 4096-block pool that the sequences
+    share: every head of six sequences against the oracle, the whole output against
+    the prefill kernel's one-token-suffix rows, and a second call bit for bit."""
+    B, ctx_len, Hq, Hkv, d = 64, 4352, 32, 8, 128
+    ctx = [ctx_len] * B
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=71, pool_blocks=4096)
+    say("[gpu] decode full size B=64 x 4352")
+    pool = pcr.KVPool(dev(pk), dev(pv), Hkv, d)
+    qd, btd = dev(q), dev(bt)
+    cl = np.asarray(ctx, np.int32)
+    cld = dev(cl)
+    out1 = torch.zeros((B, Hq, d), dtype=torch.int16, device="cuda")
+    out2 = torch.zeros_like(out1)
+    pcr.decode_attn(qd, pool, btd, cld, cl, Hq, out1)
+    pcr.decode_attn(qd, pool, btd, cld, cl, Hq, out2)
+    ref = torch.zeros_like(out1)
+    pl = cl - 1
+    cu = np.arange(B + 1, dtype=np.int32)
+    pcr.prefix_prefill_attn(qd, pool, btd, dev(pl), dev(cu), pl, cu, Hq, ref)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out2)
+    seqs = [0, 1, 17, 40, 62, 63]
+    rows = np.array([[t, h] for t in seqs for h in range(Hq)], np.int32)
+    got = synth.bf16_bits_to_f32(u16(out1)).astype(np.float64)
+    _check(got[rows[:, 0], rows[:, 1]], _decode_oracle(q, pk, pv, bt, ctx, Hkv, rows=rows), "decode full sampled")
+    # both kernels are within the tolerance of the oracle; against each other the
+    # bound is twice that
+    diff = np.abs(got - synth.bf16_bits_to_f32(u16(ref)).astype(np.float64))
+    say(f"    decode vs prefill kernel: max_abs={diff.max():.3e} mean_abs={diff.mean():.3e}")
+    assert diff.max() <= 2 * MAX_ABS and diff.mean() <= MEAN_ABS
 
 
 def test_mixed_prefill_and_decode_rows():
@@ -76,10 +214,15 @@ def test_decode_loop_16_steps():
         pl = np.asarray(ctx, np.int32)
         cu = np.arange(B + 1, dtype=np.int32)
         pcr.prefix_prefill_attn(dev(q), L.pool, bt_dev, dev(pl), dev(cu), pl, cu, Hq, out)
+        out_dec = torch.zeros_like(out)
+        n_keys = pl + 1
+        pcr.decode_attn(dev(q), L.pool, bt_dev, dev(n_keys), n_keys, Hq, out_dec)
         torch.cuda.synchronize()
         odm.append(pk, pv, kn, vn, slots, BS)
         want = oattn.attention(q, pk, pv, b.block_tables, pl, cu, Hkv, BS)
         got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
         _check(got, want, f"decode step {step}")
+        got = synth.bf16_bits_to_f32(u16(out_dec)).astype(np.float64)
+        _check(got, want, f"decode step {step} (decode entry point)")
     assert np.array_equal(u16(L.pool.k), pk) and np.array_equal(u16(L.pool.v), pv)
     assert all(t <= b.block_tables.shape[1] * BS for t in total)
