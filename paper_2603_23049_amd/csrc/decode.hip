@@ -18,8 +18,8 @@
 //   O^T[d][h]  += V^T P^T   A = 16 dims x 32 keys of V^T,    B = P^T (registers)
 // No operand is shared between waves, so K and V go from HBM straight into
 // registers: K is key-major and V d-major inside each pool block, so every A
-// operand is one 16-byte run. Two register sets alternate: the loads of the
-// next 32 keys are in flight while the current ones are used. Lane (c, q4)
+// operand is one 16-byte run. Three register sets rotate: the loads of the next
+// 64 keys are in flight while the current 32 are used. Lane (c, q4)
 // (c = lane % 16, q4 = lane / 16) loads key row 8*(c/4) + 4r + c%4 for the r-th
 // K product, so that its eight scores are keys 8*q4 .. 8*q4 + 7 of the step,
 // which are exactly its eight P^T operand values in the V product: the
@@ -52,9 +52,9 @@ constexpr int kWaves = 4;              // tasks (waves) per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kStepKeys = 32;          // keys per step: two pool blocks
 constexpr int kMaxCols = 16;           // query heads per kv head held by one tile
-// Waves per CU the split count aims at. The kernel's registers allow two per SIMD
-// (four for d = 64), but one wave per SIMD, each with two steps of loads in flight,
-// streams K/V from HBM faster than two.
+// Waves per CU the split count aims at: one per SIMD, each with three register sets
+// of K/V loads (two steps in flight while a third is used), measured faster than
+// two waves per SIMD with two sets each.
 constexpr int waves_per_cu(int) { return 4; }
 constexpr int kMinChunk = 256;         // keys; shorter chunks spend more on set-up than on loads
 constexpr float kLog2e = 1.4426950408889634f;
@@ -68,7 +68,7 @@ struct StepRegs {
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_split_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) void decode_split_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
     const int32_t *__restrict__ context_lens, int32_t B, int32_t Hq, int32_t n_split, int32_t chunk,
@@ -180,26 +180,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             o[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(R.v[mt]), pb, o[mt], 0, 0, 0);
     };
 
-    // Register set ra always holds the loads of step j when an iteration starts, so
-    // every load inside the loop is unconditional and the wait before each step
-    // leaves the other set's 16 loads in flight.
     if (active) {
+        // Three register sets rotate. Every load inside the loop is unconditional (the
+        // second prologue load rereads step 0 for a one-step chunk), so the wait before
+        // each step leaves the two later steps' loads in flight.
         const int n_steps = (kend - kbeg + kStepKeys - 1) / kStepKeys;
-        StepRegs<D> ra, rb;
+        StepRegs<D> ra, rb, rc;
         load_step(0, ra);
+        load_step(min(1, n_steps - 1), rb);
         int j = 0;
-        for (; j + 2 < n_steps; j += 2) {
-            load_step(j + 1, rb);
+        for (; j + 4 < n_steps; j += 3) {
+            load_step(j + 2, rc);
             process(j, ra);
-            load_step(j + 2, ra);
+            load_step(j + 3, ra);
             process(j + 1, rb);
+            load_step(j + 4, rb);
+            process(j + 2, rc);
         }
-        if (j + 1 < n_steps) {
-            load_step(j + 1, rb);
+        const int left = n_steps - j;               // 1 .. 4; ra holds step j, rb step j + 1
+        if (left == 1) {
+            process(j, ra);
+        } else if (left == 2) {
             process(j, ra);
             process(j + 1, rb);
-        } else {
+        } else if (left == 3) {
+            load_step(j + 2, rc);
             process(j, ra);
+            process(j + 1, rb);
+            process(j + 2, rc);
+        } else {
+            load_step(j + 2, rc);
+            process(j, ra);
+            load_step(j + 3, ra);
+            process(j + 1, rb);
+            process(j + 2, rc);
+            process(j + 3, ra);
         }
     }
 
