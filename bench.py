@@ -522,6 +522,8 @@ def main(argv=None):
     ap.add_argument("--pipeline-method", default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="only run the decode-step measurement and print its JSON")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -537,6 +539,9 @@ def main(argv=None):
     pcr.lib()   # fails loudly if libpcr.so is missing
     if args.copy_calibration:
         copy_calibration()
+        return 0
+    if args.decode_only:
+        print(json.dumps({"decode": measure_decode()}), flush=True)
         return 0
 
     batch = workload(args.workload)
