@@ -24,10 +24,12 @@
 // the second product. V is stored d-major inside each pool block, so a V^T
 // operand (8 consecutive keys of one dim) is one 16-byte LDS read.
 //
-// Softmax runs in the log2 domain with the scale folded into one FMA. The
-// running max is only raised (and O rescaled) when a tile's max exceeds it by
-// more than 2^8; otherwise the stale max stays, which keeps probabilities
-// below 256 and skips the rescale of 64 accumulators per lane.
+// Softmax runs in the log2 domain with sm_scale * log2(e) folded into Q, and
+// the first product of a tile starts from -m_ref, so the scores come out
+// already shifted. The reference max m_ref is only raised (and O rescaled)
+// when a tile's max exceeds it by more than 2^8; otherwise the stale value
+// stays, which keeps probabilities below 256 and skips the rescale of 64
+// accumulators per lane.
 //
 // Tiles move global -> LDS with global_load_lds_dwordx4 (no staging
 // registers), double-buffered with one barrier per tile. LDS chunks are
