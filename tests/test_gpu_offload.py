@@ -143,3 +143,51 @@ def test_staged_load_bitexact():
     pk, pv = pk0.copy(), pv0.copy()
     odm.load(pk, pv, data.host_k, data.host_v, L.src, L.dst)
     assert np.array_equal(u16(L.pool.k), pk) and np.array_equal(u16(L.pool.v), pv)
+
+
+@pytest.mark.parametrize("method", ["dma_staged", "kernel_pull"])
+def test_pipeline_with_offload_full_size(method):
+    """The benchmark's three-stream pipeline at full size: 32 layers of 4 sequences x
+    (4096 cached + 6144 new tokens), loads by the pull kernel, the computed whole
+    256-token chunks offloaded (96 MiB per layer) staged or by the push kernel; four
+    distinct layer data sets used round-robin, every layer with its own pool (poisoned
+    with NaN bit patterns), output and marker-filled host destination. Every layer's
+    offloaded blocks equal the oracle's bit for bit (unlisted blocks keep the marker)
+    and every output equals its data set's serialized result."""
+    b = synth.l8b_pipe32(6144)
+    n, distinct = b.num_layers, 4
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    poison = np.full(shape, NAN_BITS, np.uint16)
+    src, dst = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, BS, 256)
+    n_blocks = len(src)
+    assert n_blocks * BS * b.num_kv_heads * b.head_dim * 2 * 2 == 96 << 20
+    say(f"[gpu] pipeline with offload {b.name}: {n} layers, offload {method}")
+    base = [GpuLayer(b, synth.make_layer(b, l), poison, poison) for l in range(distinct)]
+    serial = []
+    for L in base:
+        L.run_serial("kernel_pull")
+        serial.append(L.out.clone())
+        L.pool.k.fill_(int(NAN_BITS))
+        L.pool.v.fill_(int(NAN_BITS))
+        L.out.zero_()
+    ios = [L.layer_io() for L in base]
+    for l in range(distinct, n):
+        s_ = base[l % distinct]
+        pool = pcr.KVPool(torch.full(shape, int(NAN_BITS), dtype=torch.int16, device="cuda"),
+                          torch.full(shape, int(NAN_BITS), dtype=torch.int16, device="cuda"), b.num_kv_heads,
+                          b.head_dim)
+        ios.append(pcr.Layer(s_.host, pool, s_.q, s_.k_new, s_.v_new, torch.zeros_like(s_.out)))
+    outs = [_host_out(b, n_blocks) for _ in range(n)]
+    ws = torch.empty(pcr.staged_workspace_bytes(n_blocks, b.num_kv_heads, b.head_dim), dtype=torch.uint8,
+                     device="cuda")
+    torch.cuda.synchronize()
+    cs, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    pcr.pipeline_run_offload(ios, outs, base[0].batch_plan(), src, dst, cs, ks, os_, method="kernel_pull",
+                             offload_method=method, workspace=ws)
+    torch.cuda.synchronize()
+    for k in range(distinct):
+        hk, hv = _want(b, synth.make_layer(b, k), poison, poison, src, dst, n_blocks)
+        for l in range(k, n, distinct):
+            assert torch.equal(ios[l].out, serial[k]), f"layer {l}: output differs from serial"
+            assert np.array_equal(u16(outs[l].k), hk), f"layer {l}: offloaded K"
+            assert np.array_equal(u16(outs[l].v), hv), f"layer {l}: offloaded V"
