@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
     const bool active = kbeg < n_keys;             // wave-uniform
     if (!active && !lds_merge) return;             // a merging wave stays for the barrier
     const int kend = min(n_keys, kbeg + chunk);
-    const int last_blk = min((n_keys - 1) >> 4, max_blocks - 1);   // last logical block with a visible key
+    const int last_blk = max(0, min((n_keys - 1) >> 4, max_blocks - 1));   // last block with a visible key
     const int G = Hq / Hkv;
     const int c = lane & 15, q4 = lane >> 4;
     const bool col = c < G;
