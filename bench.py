@@ -183,21 +183,44 @@ def _attn(L, bp, stream=None):
                             bp.host_cu_suffix, bp.num_q_heads, L.out, sm_scale=bp.sm_scale, stream=stream)
 
 
-def measure_step(batch, steps, warmup):
+def warm_up(fn, min_ms, min_calls=3):
+    """Calls fn until at least min_calls calls and min_ms of wall time have passed. After
+    an idle gap the GPU clock starts low and ramps up under sustained load: with 10
+    warm-up steps the l8b_layer step measured about 10% slower than after 200-1600
+    (72.2-72.8 us per step from 200 on)."""
+    import torch
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        fn()
+        n += 1
+        if n >= min_calls and n % 4 == 0:
+            torch.cuda.synchronize()
+            if (time.perf_counter() - t0) * 1e3 >= min_ms:
+                return n
+
+
+def measure_step(batch, steps, warmup, min_warm_ms=0.0):
     """Timed compute step (append + attention) with prefix KV already in the pool: one
     event pair and the wall clock around all `steps` steps, synchronized on both sides
     (an event pair per step would put its own gaps between the steps: about 7 us per
-    step measured). Then the attention and append kernels alone, back to back, for
-    their per-launch time."""
+    step measured), after `warmup` steps and, with min_warm_ms, at least that much
+    warm-up time. Then the attention and append kernels alone, back to back, for their
+    per-launch time."""
     import torch
     from paper_2603_23049_amd import pcr
     L, bp, _ = _setup_layer(batch)
     pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="kernel_pull")
     torch.cuda.synchronize()
     s = torch.cuda.current_stream()
-    for _ in range(warmup):
+    def step():
         pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
         _attn(L, bp, s)
+
+    for _ in range(warmup):
+        step()
+    if min_warm_ms > 0:
+        warm_up(step, min_warm_ms)
     torch.cuda.synchronize()
     a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -267,10 +290,30 @@ def measure_load(batch, reps=10):
     return out
 
 
+def _bracketed_ms(run, start_stream, end_stream, reps):
+    """Best of `reps` runs of `run()` after one warm-up, each timed by one event pair:
+    the start recorded on start_stream before the call, the end on end_stream after it
+    (the pipelines' own per-layer events add gaps to the streams they sit on, so the
+    totals come from untimed runs)."""
+    import torch
+    times = []
+    for r in range(reps + 1):
+        torch.cuda.synchronize()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(start_stream)
+        run()
+        e.record(end_stream)
+        e.synchronize()
+        if r >= 1:
+            times.append(a.elapsed_time(e))
+    return min(times)
+
+
 def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinct=None):
     """The n-layer two-stream pipeline. Exposure per layer is the pipeline's time per
     layer beyond the layer's isolated compute; its least possible value follows from
-    the isolated per-layer load and compute times (two in-order queues). With
+    the isolated per-layer load and compute times (two in-order queues). The total
+    comes from untimed runs; one timed run gives the per-layer breakdown. With
     `distinct`, only that many layers' host/Q/K/V data are generated and reused
     round-robin (every layer still has its own pool and moves its own bytes)."""
     import torch
@@ -278,18 +321,15 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
     n = batch.num_layers
     layers, bp = _setup_pipeline(batch, distinct or n)
     copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
-    runs = []
-    for r in range(reps + 1):
-        t = pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method, timing=True)
-        if r >= 1:
-            runs.append(t)
-    best = min(runs, key=lambda t: t["total_ms"])
-    e_raw = best["total_ms"] / n - compute_ms_iso
+    total = _bracketed_ms(lambda: pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method), comp_s, comp_s,
+                          reps)
+    best = pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method, timing=True)
+    e_raw = total / n - compute_ms_iso
     e_min = flow_shop_exposure(load_ms_iso, compute_ms_iso, n) / n
     del layers
     torch.cuda.synchronize()
     return {"layers": n, "workload": batch.name, "method": method, "distinct_layer_data": distinct or n,
-            "total_ms": best["total_ms"],
+            "total_ms": total, "total_ms_timed_run": best["total_ms"],
             "sum_compute_ms_in_pipeline": best["sum_compute_ms"],
             "load_ms_per_layer_isolated": load_ms_iso, "compute_ms_per_layer_isolated": compute_ms_iso,
             "load_ms_per_layer_in_pipeline": float(np.median(best["load_ms"])),
@@ -330,8 +370,7 @@ def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
     s = torch.cuda.current_stream()
 
     def timed(fn):
-        for _ in range(3):
-            fn()
+        warm_up(fn, 30.0)
         a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(s)
         for _ in range(steps):
@@ -463,20 +502,19 @@ def measure_pipeline_offload(batch, method, load_ms_iso, compute_ms_iso, offload
     cs, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     ws = torch.empty(pcr.staged_workspace_bytes(len(src), batch.num_kv_heads, batch.head_dim), dtype=torch.uint8,
                      device="cuda")
-    runs = []
-    for r in range(reps + 1):
-        t = pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
-                                     offload_method=offload_method, workspace=ws, timing=True)
-        if r >= 1:
-            runs.append(t)
-    best = min(runs, key=lambda t: t["total_ms"])
-    e_raw = best["total_ms"] / n - compute_ms_iso
+    total = _bracketed_ms(lambda: pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
+                                                           offload_method=offload_method, workspace=ws),
+                          ks, os_, reps)
+    best = pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
+                                    offload_method=offload_method, workspace=ws, timing=True)
+    e_raw = total / n - compute_ms_iso
     bound = flow_shop3_makespan(load_ms_iso, compute_ms_iso, offload_ms_iso, n)
     e_min = bound / n - compute_ms_iso
     del layers, outs, dsts
     torch.cuda.synchronize()
     return {"layers": n, "workload": batch.name, "method": method, "offload_method": offload_method,
-            "distinct_layer_data": distinct, "total_ms": best["total_ms"], "compute_end_ms": best["compute_end_ms"],
+            "distinct_layer_data": distinct, "total_ms": total, "total_ms_timed_run": best["total_ms"],
+            "compute_end_ms": best["compute_end_ms"],
             "load_ms_per_layer_isolated": load_ms_iso, "compute_ms_per_layer_isolated": compute_ms_iso,
             "offload_ms_per_layer_isolated": offload_ms_iso,
             "offload_ms_per_layer_in_pipeline": float(np.median(best["offload_ms"])),
@@ -514,8 +552,10 @@ def cpu_baseline(batch, budget_s=12.0):
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=400,
+                    help="untimed steps first; the GPU clock needs about 200 l8b_layer steps (15 ms) "
+                         "of sustained load to settle")
     ap.add_argument("--workload", default="l8b_layer")
     ap.add_argument("--no-pipeline", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -578,7 +618,7 @@ def main(argv=None):
         extra["decode"] = measure_decode()
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
-        rst = measure_step(rb, max(10, args.steps // 2), 3)
+        rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=50.0)
         rfl = attention_flops(rb.prefix_lens, rb.suffix_lens, rb.num_q_heads, rb.head_dim)
         extra["rag_mix"] = {"attn_ms": rst["attn_ms"], "step_ms": rst["step_ms"], "flops": rfl,
                             "attn_tflops": rfl / (rst["attn_ms"] * 1e-3) / 1e12,
@@ -592,7 +632,7 @@ def main(argv=None):
             extra["offload"] = off
             for pb in (synth.l70b_pipe80(), synth.l8b_pipe32(suffix=6144)):
                 _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, 4 distinct layer data sets)")
-                pst = measure_step(pb, 10, 3)
+                pst = measure_step(pb, 10, 3, min_warm_ms=50.0)
                 pld = measure_load(pb, reps=4)
                 pipelines[pb.name] = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"],
                                                       reps=2, distinct=4)
