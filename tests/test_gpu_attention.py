@@ -56,10 +56,11 @@ def test_tiny_config_full():
 
 
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("G", [1, 4, 8])
+@pytest.mark.parametrize("G", [1, 2, 4, 5, 8, 16])
 def test_edge_shapes(d, G):
     """p in {0,1,15,16,17,256}, s in {1,2,63,64} (all combinations in one ragged batch
-    per (d, G)), plus a long ragged suffix spanning several row tiles."""
+    per (d, G)), plus a long ragged suffix spanning several row tiles. Row tiles hold
+    128 packed (token, head) rows, so G = 5 puts tile edges inside a token's heads."""
     pl, sl = [], []
     for p in [0, 1, 15, 16, 17, 256]:
         for s in [1, 2, 63, 64]:
