@@ -181,3 +181,20 @@ def test_rag_mix_sampled_rows_and_pool():
                            b.num_kv_heads, BS, rows=rows)
     got = L.out_f64()[rows[:, 0], rows[:, 1]]
     _check(got, want, "rag_mix sampled")
+
+
+def test_long_context_128k_sampled_rows():
+    """One sequence with a 131072-token cached prefix and 256 new tokens (32 q / 8 kv
+    heads, d = 128): 2052 key tiles per row tile, so the online softmax runs over
+    131k keys in fp32. Sampled rows of every eighth head against the fp64 oracle."""
+    b = synth.ragged_batch("long128k", Hq=32, Hkv=8, d=128, prefix_lens=[131072], suffix_lens=[256],
+                           pool_blocks=8256, seed=77)
+    data = synth.make_layer(b)
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    zero = np.zeros(shape, np.uint16)
+    say("[gpu] attention 128k-token prefix (sampled rows)")
+    L = _run(b, data, zero, zero)
+    rows = np.array([[t, h] for t in (0, 1, 127, 128, 254, 255) for h in range(0, 32, 8)], np.int32)
+    want = _oracle(b, data, zero, zero, rows=rows)
+    got = L.out_f64()[rows[:, 0], rows[:, 1]]
+    _check(got, want, "128k prefix")

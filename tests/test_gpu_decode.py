@@ -94,6 +94,19 @@ def test_decode_ragged_merged_in_workgroup(B, d):
     _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode merged B={B} d={d}")
 
 
+def test_decode_long_contexts():
+    """Contexts of 131072 and 65537 keys (two sequences): 64 and 33 chunks of 2048 keys
+    merged through the workspace (the last one holding a single key), fp32 sums over
+    131k keys."""
+    ctx = [131072, 65537]
+    Hq, Hkv, d = 32, 8, 128
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=13)
+    say(f"[gpu] decode long contexts {ctx} workspace={pcr.decode_attn_workspace_bytes(2, Hq, Hkv, d, max(ctx))}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), "decode long contexts")
+
+
 def test_decode_many_short_sequences_without_workspace():
     """300 sequences of 1-300 keys: one chunk each, so no workspace is needed or passed."""
     rng = np.random.Generator(np.random.PCG64(5))
