@@ -183,6 +183,100 @@ def _attn(L, bp, stream=None):
                             bp.host_cu_suffix, bp.num_q_heads, L.out, sm_scale=bp.sm_scale, stream=stream)
 
 
+class ClockSampler:
+    """amd-smi clock and power samples. The sampling shell is started before this
+    process touches the GPU (a process that has initialised the GPU starts no other
+    program) and waits on a pipe until start() tells it to begin."""
+
+    def __init__(self, n=6, period_s=0.25):
+        import shutil
+        import subprocess
+        self.proc = None
+        smi = shutil.which("amd-smi")
+        if smi is None:
+            return
+        script = (f"read go || exit 0; for i in $(seq 1 {n}); do echo @sample; "
+                  f"timeout 5 {smi} metric -g 0 --clock --power --json 2>/dev/null; sleep {period_s}; done")
+        self.proc = subprocess.Popen(["bash", "-c", script], stdin=subprocess.PIPE, stdout=subprocess.PIPE,
+                                     stderr=subprocess.DEVNULL, text=True)
+
+    def start(self):
+        if self.proc:
+            self.proc.stdin.write("go\n")
+            self.proc.stdin.flush()
+
+    def running(self):
+        return self.proc is not None and self.proc.poll() is None
+
+    def collect(self, timeout=30):
+        """[(gfx MHz per XCD, socket power W)] of the samples that parsed."""
+        if self.proc is None:
+            return []
+        try:
+            out, _ = self.proc.communicate(timeout=timeout)
+        except Exception:
+            self.proc.kill()
+            return []
+        samples = []
+        for body in out.split("@sample")[1:]:
+            try:
+                g = json.loads(body)["gpu_data"][0]
+                clk = g["clock"]
+                gfx = [clk[k]["clk"]["value"] for k in sorted(clk) if k.startswith("gfx_")]
+                samples.append((gfx, g["power"]["socket_power"]["value"]))
+            except Exception:
+                continue
+        return samples
+
+    def close(self):
+        if self.proc and self.proc.poll() is None:
+            try:
+                self.proc.stdin.close()
+                self.proc.wait(timeout=10)
+            except Exception:
+                self.proc.kill()
+
+
+def measure_clock_hold(batch, sampler, settle_s=0.5, max_s=15.0):
+    """The attention kept running back to back while amd-smi samples the clocks and the
+    socket power (after settle_s of load). Returns the samples' per-XCD mean clocks, their
+    mean, the mean power and the attention time per launch during the sampling."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    if sampler.proc is None:
+        return None
+    L, bp, _ = _setup_layer(batch)
+    pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="kernel_pull")
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    t0 = time.perf_counter()
+    started = False
+    launches, ms = 0, 0.0
+    while time.perf_counter() - t0 < max_s:
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(50):
+            _attn(L, bp, s)
+        e.record(s)
+        e.synchronize()
+        if started:
+            launches += 50
+            ms += a.elapsed_time(e)
+            if not sampler.running():
+                break
+        elif time.perf_counter() - t0 >= settle_s:
+            sampler.start()
+            started = True
+    samples = sampler.collect()
+    if not samples or launches == 0:
+        return None
+    n_x = min(len(g) for g, _ in samples)
+    per_xcd = [float(np.mean([g[x] for g, _ in samples])) for x in range(n_x)]
+    return {"gfx_mhz_per_xcd": per_xcd, "gfx_mhz_mean": float(np.mean(per_xcd)),
+            "gfx_mhz_min": float(min(per_xcd)), "socket_power_w": float(np.mean([p for _, p in samples])),
+            "samples": len(samples), "attn_ms_during": ms / launches, "source": "amd-smi metric --clock --power"}
+
+
 def warm_up(fn, min_ms, min_calls=3):
     """Calls fn until at least min_calls calls and min_ms of wall time have passed. After
     an idle gap the GPU clock starts low and ramps up under sustained load: with 10
@@ -574,6 +668,15 @@ def main(argv=None):
               "has one GPU; run with --gpus 1", file=sys.stderr)
         return 2
 
+    sampler = ClockSampler() if not (args.copy_calibration or args.decode_only) else None
+    try:
+        return _main(args, sampler)
+    finally:
+        if sampler:
+            sampler.close()
+
+
+def _main(args, sampler):
     import torch
     from paper_2603_23049_amd import pcr, synth
     if not torch.cuda.is_available():
@@ -595,6 +698,8 @@ def main(argv=None):
     attn_tflops = flops / (st["attn_ms"] * 1e-3) / 1e12
     app_b = append_bytes(batch.T, batch.num_kv_heads, batch.head_dim)
     _say(f"[bench] step {st['step_ms']:.4f} ms, attention {st['attn_ms']:.4f} ms = {attn_tflops:.1f} TFLOP/s")
+    _say("[bench] clocks under the attention (amd-smi)")
+    clocks = measure_clock_hold(batch, sampler)
 
     load = None
     if not args.no_load:
@@ -671,7 +776,13 @@ def main(argv=None):
         "mfma_frac": value / MFMA_BF16_PEAK_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": "prefill_attn_kernel", "achieved": attn_tflops,
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
-                     "traffic": measured_traffic(), "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"]},
+                     "traffic": measured_traffic(), "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"],
+                     "sampled_clock_mhz": clocks["gfx_mhz_mean"] if clocks else None,
+                     "peak_at_sampled_clock": (MFMA_BF16_PEAK_TFLOPS * clocks["gfx_mhz_mean"] / 2400.0
+                                               if clocks else None),
+                     "frac_at_sampled_clock": (attn_tflops / (MFMA_BF16_PEAK_TFLOPS * clocks["gfx_mhz_mean"] / 2400.0)
+                                               if clocks else None)},
+        "clocks": clocks,
         "append": {"ms": st["append_ms"], "bytes": app_b, "GBps": app_b / st["append_ms"] / 1e6,
                    "frac_hbm": app_b / st["append_ms"] / 1e6 / HBM_PEAK_GBS},
         "load": load,
