@@ -243,7 +243,7 @@ def measure_clock_hold(batch, sampler, settle_s=0.5, max_s=15.0):
     mean, the mean power and the attention time per launch during the sampling."""
     import torch
     from paper_2603_23049_amd import pcr
-    if sampler.proc is None:
+    if sampler is None or sampler.proc is None:
         return None
     L, bp, _ = _setup_layer(batch)
     pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="kernel_pull")
@@ -661,6 +661,8 @@ def main(argv=None):
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
     ap.add_argument("--decode-only", action="store_true",
                     help="only run the decode-step measurement and print its JSON")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="skip the amd-smi clock samples under the attention (never taken under a profiler)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -668,7 +670,12 @@ def main(argv=None):
               "has one GPU; run with --gpus 1", file=sys.stderr)
         return 2
 
-    sampler = ClockSampler() if not (args.copy_calibration or args.decode_only) else None
+    # Under a profiler the tool library has initialised the GPU before this script runs,
+    # so no other program may be started from here: no clock sampling then.
+    under_profiler = (any(k.startswith(("ROCPROF", "ROCP_")) for k in os.environ)
+                      or "rocprof" in os.environ.get("LD_PRELOAD", ""))
+    sampler = (ClockSampler() if not (args.copy_calibration or args.decode_only or args.no_clocks or under_profiler)
+               else None)
     try:
         return _main(args, sampler)
     finally:
