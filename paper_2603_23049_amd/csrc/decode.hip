@@ -10,8 +10,9 @@
 // decode step is bound by reading K/V from HBM, not by matrix work.
 //
 // Work decomposition. The key range of each (sequence, kv head) is cut into
-// n_split chunks of `chunk` keys (a multiple of 32). Each chunk is the task of
-// one wave; the host picks n_split so that every SIMD gets about one wave. A wave holds the G query heads of its kv head as the columns of
+// n_split chunks of `chunk` keys (a multiple of 32). Each chunk is the work of
+// one wave; the host picks n_split so that every SIMD gets about one wave. A
+// wave holds the G query heads of its kv head as the columns of
 // v_mfma_f32_16x16x32_bf16 tiles (G <= 16) and walks its chunk 32 keys (two
 // pool blocks) at a time:
 //   S^T[key][h] = K Q^T     A = 16 key rows x 32 dims of K,  B = Q^T (registers)
