@@ -121,6 +121,18 @@ def test_decode_many_short_sequences_without_workspace():
     _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), "decode short")
 
 
+def test_decode_workspace_size_is_monotone():
+    """A workspace sized for max_context serves every batch of the same size whose
+    contexts are shorter: the size never decreases as max_context grows (host only,
+    the query reads the device's compute-unit count)."""
+    lens = [1, 2, 16, 31, 255, 256, 257, 300, 511, 1000, 1088, 2176, 4352, 4353, 16384, 131072]
+    for B, Hq, Hkv, d in [(1, 32, 8, 128), (2, 32, 8, 128), (8, 64, 8, 128), (16, 16, 1, 64), (64, 32, 8, 128),
+                          (512, 32, 8, 128)]:
+        sizes = [pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, n) for n in lens]
+        assert all(a <= b for a, b in zip(sizes, sizes[1:])), (B, Hq, Hkv, d, sizes)
+        assert sizes[0] == 0
+
+
 def test_decode_workspace_checked():
     """A workspace smaller than the batch needs is refused before anything is enqueued."""
     ctx = [4000, 3000]
