@@ -661,6 +661,9 @@ def main(argv=None):
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
     ap.add_argument("--decode-only", action="store_true",
                     help="only run the decode-step measurement and print its JSON")
+    ap.add_argument("--pipeline-only", action="store_true",
+                    help="only run the 32-layer pipeline (with its isolated load and compute times) and print "
+                         "its JSON")
     ap.add_argument("--no-clocks", action="store_true",
                     help="skip the amd-smi clock samples under the attention (never taken under a profiler)")
     args = ap.parse_args(argv)
@@ -674,8 +677,8 @@ def main(argv=None):
     # so no other program may be started from here: no clock sampling then.
     under_profiler = (any(k.startswith(("ROCPROF", "ROCP_")) for k in os.environ)
                       or "rocprof" in os.environ.get("LD_PRELOAD", ""))
-    sampler = (ClockSampler() if not (args.copy_calibration or args.decode_only or args.no_clocks or under_profiler)
-               else None)
+    sampler = (ClockSampler() if not (args.copy_calibration or args.decode_only or args.pipeline_only or args.no_clocks
+                                      or under_profiler) else None)
     try:
         return _main(args, sampler)
     finally:
@@ -695,6 +698,14 @@ def _main(args, sampler):
         return 0
     if args.decode_only:
         print(json.dumps({"decode": measure_decode()}), flush=True)
+        return 0
+    if args.pipeline_only:
+        pb = synth.l8b_pipe32()
+        pst = measure_step(pb, args.steps, args.warmup)
+        pld = measure_load(pb)
+        method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
+        print(json.dumps({"pipeline": measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"]),
+                          "load": pld, "step_ms": pst["step_ms"]}), flush=True)
         return 0
 
     batch = workload(args.workload)
