@@ -24,12 +24,15 @@
 // the second product. V is stored d-major inside each pool block, so a V^T
 // operand (8 consecutive keys of one dim) is one 16-byte LDS read.
 //
-// Softmax runs in the log2 domain with sm_scale * log2(e) folded into Q, and
-// the first product of a tile starts from -m_ref, so the scores come out
-// already shifted. The reference max m_ref is only raised (and O rescaled)
-// when a tile's max exceeds it by more than 2^8; otherwise the stale value
-// stays, which keeps probabilities below 256 and skips the rescale of 64
-// accumulators per lane.
+// Softmax runs in the log2 domain. The first product of a tile starts from
+// -m_ref, so the raw scores <q, k> come out already shifted, and one fp32
+// multiply by c = sm_scale * log2(e) precedes each exp2. (Folding c into Q
+// instead would round q*c to bf16: a relative error of 2^-9 on every score,
+// which for sharp rows of large |<q, k>| moves the output by far more than the
+// bf16 inputs themselves do.) The reference max m_ref is only raised (and O
+// rescaled) when a tile's scaled max exceeds it by more than 8, i.e. a factor
+// of 2^8; otherwise the stale value stays, which keeps probabilities below 256
+// and skips the rescale of 64 accumulators per lane.
 //
 // Tiles move global -> LDS with global_load_lds_dwordx4 (no staging
 // registers), double-buffered with one barrier per tile. LDS chunks are
@@ -61,7 +64,7 @@ constexpr int kThreads = 2 * kGroupWaves * 64;           // 512
 constexpr int kTileKeys = 64;
 constexpr int kTileBlocks = kTileKeys / kBlockSize;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kRescaleThreshold = 8.0f;                // log2 units
+constexpr float kRescaleThreshold = 8.0f;                // log2 units: P <= 2^8
 #ifndef KAHEAD
 #define KAHEAD 6
 #endif
@@ -163,7 +166,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
     const int32_t *__restrict__ prefix_lens, const int32_t *__restrict__ cu_suffix, int32_t Hq,
-    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, u16 *__restrict__ out, const AttnWorkMap wm)
+    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, float rescale_thr, u16 *__restrict__ out,
+    const AttnWorkMap wm)
 {
     using Geo = TileGeom<D>;
     constexpr int CPR = Geo::CPR;
@@ -280,11 +284,13 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o_acc[mt][r] = 0.f;
-    // Scores are kept relative to a reference m_ref (log2 domain): the first product
-    // starts from -m_ref, so S^T holds scale*log2(e)*<q,k> - m_ref and P = exp2(S^T).
+    // Scores are kept relative to a reference m_ref (raw units of <q,k>): the first
+    // product starts from -m_ref, so S^T holds <q,k> - m_ref and P = exp2(c * S^T) with
+    // c = scale_log2.
     float m_ref = 0.f;
     // The reference moves when a tile's max (relative to it) exceeds thr: -inf until the
-    // first real score of the row, then 2^8, so P stays <= 256 and O is rescaled rarely.
+    // first real score of the row, then rescale_thr = 8 / c, so P stays <= 2^8 and O is
+    // rescaled rarely.
     float thr = -INFINITY;
     float l_run[2] = {0.f, 0.f};   // this lane's part of the denominator (two chains)
     f32x16 nbias;
@@ -457,7 +463,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         __builtin_amdgcn_s_setprio(0);
     };
 
-    // ---- vector work: online softmax of S^T(j) into bf16 P(j) (log2 domain, lazy rescale) ----
+    // ---- vector work: online softmax of S^T(j) into bf16 P(j) (lazy rescale) ----
     auto softmax = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
         const int kbase = (tile_begin + j) * kTileKeys;
         if (kbase + kTileKeys - 1 > w_min_limit) {
@@ -470,23 +476,35 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                     st[m][r] = (32 * m + 16 * (r >> 3) + (r & 7)) > lim ? -INFINITY : st[m][r];
         }
         // NaN-propagating maximum (v_maximum3_f32): unlike fmaxf it needs no
-        // canonicalisation of the MFMA results, one instruction per two scores.
-        float mx = -INFINITY;
+        // canonicalisation of the MFMA results. Written as two chains of
+        // max(max(m, a), b), one three-operand instruction per two scores; a pairwise
+        // tree would spend a three-operand instruction on every pair.
+        float mc[2];
 #pragma unroll
-        for (int m = 0; m < 2; ++m)
+        for (int m = 0; m < 2; ++m) {
+            mc[m] = __builtin_elementwise_maximum(st[m][0], st[m][1]);
 #pragma unroll
-            for (int r = 0; r < 16; r += 2)
-                mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(st[m][r], st[m][r + 1]));
-        {   // the other half-wave holds the other 32 keys of the same query
-            const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
-                                                             __builtin_bit_cast(unsigned, mx), false, false);
-            mx = __builtin_elementwise_maximum(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+            for (int r = 2; r < 16; r += 2)
+                mc[m] = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mc[m], st[m][r]), st[m][r + 1]);
+        }
+        float mx = __builtin_elementwise_maximum(mc[0], mc[1]);
+        {   // The other half-wave holds the other 32 keys of the same query: swap halves and
+            // take the larger. The two swap results are copied out of the returned vector
+            // before the bit casts: a bit cast applied to an element of it directly reads
+            // element 0 for both, which drops the half-wave's own keys from its max.
+            const unsigned mine = __builtin_bit_cast(unsigned, mx);
+            const auto sw = __builtin_amdgcn_permlane32_swap(mine, mine, false, false);
+            const unsigned lo = sw[0], hi = sw[1];
+            mx = __builtin_elementwise_maximum(__builtin_bit_cast(float, lo), __builtin_bit_cast(float, hi));
         }
         const bool need = mx > thr;
         if (__builtin_amdgcn_ballot_w64(need)) {
             const float delta = need ? mx : 0.f;
-            const float alpha = __builtin_amdgcn_exp2f(-delta);
-            thr = need ? kRescaleThreshold : thr;
+            // Before a row's first real score nothing has accumulated, and that first max
+            // may lie far below the initial reference (2^-delta would overflow to +inf
+            // and turn the zero accumulators into NaN): scale by 0 then.
+            const float alpha = thr == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(-delta * scale_log2);
+            thr = need ? rescale_thr : thr;
             m_ref += delta;
             l_run[0] *= alpha;
             l_run[1] *= alpha;
@@ -501,19 +519,23 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) nbias[r] = -m_ref;
         }
-        // Row sums from the fp32 probabilities with plain adds: the bf16 dot instructions
-        // would serve the same purpose in half the count, but they wait behind the other
-        // wave's MFMAs on this SIMD (measured about 70 cycles each), while VALU adds issue
-        // beside them.
+        // Row sums of the bf16-rounded probabilities, the same values the second product
+        // weights V with: the weights then sum to one however P rounds (a one-hot row
+        // returns its V row exactly), where a sum of the fp32 values would leave up to
+        // 2^-8 of relative error on a dominant term. Plain VALU adds: the bf16 dot
+        // instructions would need half the count, but they wait behind the other wave's
+        // MFMAs on this SIMD (measured about 70 cycles each), while the adds issue beside
+        // them.
 #pragma unroll
         for (int t = 0; t < kTileBlocks; ++t) {
             f32x8 pv8;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                pv8[e] = __builtin_amdgcn_exp2f(st[t >> 1][8 * (t & 1) + e]);
+                pv8[e] = __builtin_amdgcn_exp2f(st[t >> 1][8 * (t & 1) + e] * scale_log2);
             pf[t] = __builtin_convertvector(pv8, bf16x8);
-            l_run[0] += (pv8[0] + pv8[1]) + (pv8[2] + pv8[3]);
-            l_run[1] += (pv8[4] + pv8[5]) + (pv8[6] + pv8[7]);
+            const f32x8 pr = __builtin_convertvector(pf[t], f32x8);
+            l_run[0] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+            l_run[1] += (pr[4] + pr[5]) + (pr[6] + pr[7]);
         }
     };
 
@@ -534,15 +556,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     tile_ids(1, ids_raw);
     to_offs(ids_raw, ids_k);
     // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row),
-    // pre-multiplied by sm_scale*log2(e) so that the first product yields log2-domain
-    // scores directly.
+    // the bf16 input as it is.
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-        f32x8 f = __builtin_convertvector(as_bf16x8(q_ok ? q_raw[ks] : u32x4{0u, 0u, 0u, 0u}), f32x8);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] *= scale_log2;
-        qf[ks] = __builtin_convertvector(f, bf16x8);
-    }
+    for (int ks = 0; ks < KSTEPS; ++ks) qf[ks] = as_bf16x8(q_ok ? q_raw[ks] : u32x4{0u, 0u, 0u, 0u});
     wait_vmem();
     __syncthreads();
 
@@ -648,8 +664,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const float m1 = ml[0], l1 = ml[1];
     const float m0 = has_ref ? m_ref : -INFINITY;
     const float mm = fmaxf(m0, m1);
-    const float a0 = (m0 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m0 - mm);
-    const float a1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
+    const float a0 = (m0 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m0 - mm) * scale_log2);
+    const float a1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m1 - mm) * scale_log2);
     const float inv = 1.f / (a0 * l_tot + a1 * l1);
     if (row_valid && tq < T) {
         u16 *orow = out + (tq * Hq + h) * D;
@@ -716,6 +732,7 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
     }
     const dim3 grid((unsigned)n_items);
     const float scale_log2 = sm_scale * kLog2e;
+    const float rescale_thr = kRescaleThreshold / scale_log2;   // in units of <q,k>
     auto *qq = static_cast<const u16 *>(q);
     auto *pk = static_cast<const u16 *>(pool.k);
     auto *pv = static_cast<const u16 *>(pool.v);
@@ -723,11 +740,11 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
     if (pool.head_dim == 128)
         hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo, wm);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
     else
         hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, dim3(kThreads), 0, s, qq, pk, pv,
                            pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, oo, wm);
+                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
     return hipGetLastError();
 }
 

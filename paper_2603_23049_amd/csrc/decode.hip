@@ -169,7 +169,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
             for (int i = 0; i < 4; ++i) {
                 const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r][i], scale_log2, -m_new));
                 pb[4 * r + i] = (__bf16)p;
-                ps += p;
+                ps += (float)pb[4 * r + i];     // the rounded value the product weights V with
             }
         l_run = l_run * alpha + ps;
         if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {   // the max rose in some column

@@ -198,3 +198,21 @@ def test_long_context_128k_sampled_rows():
     want = _oracle(b, data, zero, zero, rows=rows)
     got = L.out_f64()[rows[:, 0], rows[:, 1]]
     _check(got, want, "128k prefix")
+
+
+@pytest.mark.parametrize("scale", [0.0, 8.0, 32.0])
+def test_softmax_flat_and_sharp(scale):
+    """Queries scaled by 0 (every score equal: the output is the mean of the visible
+    values), 8 and 32 (near one-hot rows whose running max rises by more than 2^8
+    again and again, so the lazy rescale runs)."""
+    pl, sl = [0, 1, 100, 1000, 3000], [64, 300, 33, 129, 256]
+    b = synth.ragged_batch("sharp", Hq=16, Hkv=4, d=128, prefix_lens=pl, suffix_lens=sl,
+                           pool_blocks=sum(-(-(p + s) // BS) for p, s in zip(pl, sl)) + 4, seed=55)
+    data = synth.make_layer(b)
+    q = synth.bf16_bits_to_f32(data.q) * np.float32(scale)
+    data = synth.LayerData(q=synth.f32_to_bf16_bits(q), k_new=data.k_new, v_new=data.v_new, host_k=data.host_k,
+                           host_v=data.host_v)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention softmax scale x{scale}")
+    L = _run(b, data, pk0, pv0)
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"q x{scale}")

@@ -107,6 +107,20 @@ def test_decode_long_contexts():
     _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), "decode long contexts")
 
 
+@pytest.mark.parametrize("scale", [0.0, 8.0, 32.0])
+def test_decode_softmax_flat_and_sharp(scale):
+    """Queries scaled by 0 (the mean of the values), 8 and 32 (near one-hot, the
+    running max rising step after step), across the in-workgroup and workspace merges."""
+    ctx = [1, 40, 700, 3000, 4352, 9000]
+    Hq, Hkv, d = 32, 8, 128
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=21)
+    q = synth.f32_to_bf16_bits(synth.bf16_bits_to_f32(q) * np.float32(scale))
+    say(f"[gpu] decode softmax scale x{scale}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode q x{scale}")
+
+
 def test_decode_many_short_sequences_without_workspace():
     """300 sequences of 1-300 keys: one chunk each, so no workspace is needed or passed."""
     rng = np.random.Generator(np.random.PCG64(5))
