@@ -228,6 +228,11 @@ pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void 
  *   host_prefix_lens, host_cu_suffix   host copies of the same (used to size the launch;
  *                  they must equal the device arrays)
  *   out            device bf16 [T][Hq][d]; fp32 accumulation, rounded to nearest even
+ *   sm_scale       finite and > 0 (else PCR_ERR_INVALID_ARG)
+ * Numerics: scores <q, k_j> and their scaling are fp32; the probabilities enter the
+ * product with V rounded to bf16 and each row is normalised by the sum of those
+ * rounded values, so the weights sum to one for any softmax sharpness. Per output
+ * element the error is about 2^-8 max_j |v_j - out| plus half a bf16 ulp of out.
  * Every key position j <= p_b + s_b - 1 must hold valid data (loaded or appended);
  * slots past p_b + s_b are never read into the result.
  */
@@ -259,7 +264,9 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
  *                      need their own.
  * The key range of each (sequence, kv head) is split into chunks processed in
  * parallel and merged exactly (a second kernel on the same stream), so the
- * result does not depend on the split beyond fp32 rounding.
+ * result does not depend on the split beyond fp32 rounding. Numerics as for
+ * pcr_prefix_prefill_attn (fp32 scores, bf16 probabilities, rows normalised by
+ * the rounded values); sm_scale must be finite and > 0.
  * Errors: PCR_ERR_UNSUPPORTED if Hq/Hkv > 16 (pcr_prefix_prefill_attn with
  * one-token suffixes covers that case); PCR_ERR_INVALID_ARG if some n_b < 1,
  * ceil(n_b/bs) > max_blocks, or the workspace is missing or too small (the
