@@ -343,6 +343,12 @@ typedef struct pcr_batch {
  * queue run in series. Create these streams before others, or raise
  * GPU_MAX_HW_QUEUES before HIP starts (the same holds for the three streams of
  * pcr_pipeline_run_offload).
+ * Errors: the attention arguments of every layer (batch-wide lengths, heads,
+ * sm_scale, block table size; each layer's pool, q and out) are checked before
+ * anything is queued, and an error there leaves the streams untouched. A later
+ * error (a load's block list or unpinned host memory, found when that layer's
+ * load is queued; a failed launch) returns with the earlier layers' work still
+ * queued: it runs to completion, and the pools' contents are then unspecified.
  */
 pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
                             pcr_load_method method, void *copy_stream, void *compute_stream,

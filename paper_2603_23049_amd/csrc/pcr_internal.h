@@ -76,4 +76,12 @@ pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const
 // Rows of packed (token, head-in-group) queries one attention workgroup handles.
 int attn_rows_per_workgroup(int head_dim);
 
+// Every argument check of pcr_prefix_prefill_attn, with no launch (errors name `who`);
+// on success *T_out is the suffix token count (0: nothing to do) and *max_tiles_out
+// the largest row-tile count of a sequence.
+pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
+                      const int32_t *prefix_lens, const int32_t *cu_suffix, const int32_t *host_prefix_lens,
+                      const int32_t *host_cu_suffix, int32_t B, int32_t num_q_heads, float sm_scale,
+                      const void *out, const char *who, int64_t *T_out, int64_t *max_tiles_out);
+
 }  // namespace pcr

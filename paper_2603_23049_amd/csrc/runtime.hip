@@ -584,13 +584,17 @@ pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void 
     return PCR_OK;
 }
 
-pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
-                                   int32_t max_blocks, const int32_t *prefix_lens, const int32_t *cu_suffix,
-                                   const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
-                                   int32_t num_q_heads, float sm_scale, void *out, void *stream)
+}  // extern "C"
+
+namespace pcr {
+
+pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
+                      const int32_t *prefix_lens, const int32_t *cu_suffix, const int32_t *host_prefix_lens,
+                      const int32_t *host_cu_suffix, int32_t B, int32_t num_q_heads, float sm_scale,
+                      const void *out, const char *who, int64_t *T_out, int64_t *max_tiles_out)
 {
-    g_err[0] = 0;
-    const char *who = "pcr_prefix_prefill_attn";
+    *T_out = 0;
+    *max_tiles_out = 0;
     pcr_status st = check_pool(pool, who);
     if (st) return st;
     if (B < 0) return fail(PCR_ERR_INVALID_ARG, "%s: B < 0", who);
@@ -623,6 +627,26 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const
         return fail(PCR_ERR_INVALID_ARG, "%s: q/out must be 16-byte aligned", who);
     if (max_tiles * pool->num_kv_heads * (int64_t)B > (int64_t)1 << 30)
         return fail(PCR_ERR_UNSUPPORTED, "%s: batch too large for one launch", who);
+    *T_out = T;
+    *max_tiles_out = max_tiles;
+    return PCR_OK;
+}
+
+}  // namespace pcr
+
+extern "C" {
+
+pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                                   int32_t max_blocks, const int32_t *prefix_lens, const int32_t *cu_suffix,
+                                   const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
+                                   int32_t num_q_heads, float sm_scale, void *out, void *stream)
+{
+    g_err[0] = 0;
+    int64_t T = 0, max_tiles = 0;
+    pcr_status st = attn_check(q, pool, block_tables, max_blocks, prefix_lens, cu_suffix, host_prefix_lens,
+                               host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T,
+                               &max_tiles);
+    if (st || T == 0) return st;
     hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
                                               host_prefix_lens, host_cu_suffix, B,
                                               num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,

@@ -150,6 +150,25 @@ def test_argument_validation_before_any_device_work():
     lay = (pcr._LayerIO * 1)()
     bat = pcr._Batch()
     assert L.pcr_pipeline_run(lay, 1, P(bat), 0, 0x5, 0x5, None) == pcr.PCR_ERR_INVALID_ARG
+    # the attention arguments of every layer are checked before anything is queued
+    # (the stream handles are never used on these paths)
+    lay2 = (pcr._LayerIO * 2)()
+    for i in range(2):
+        lay2[i].pool = _pool(Hkv=2)
+        lay2[i].q = lay2[i].out = 16
+    bat2 = pcr._Batch(block_tables=16, max_blocks=4, prefix_lens=16, cu_suffix=16,
+                      host_prefix_lens=hpl.ctypes.data, host_cu_suffix=hcu.ctypes.data, B=1, num_q_heads=4,
+                      sm_scale=0.0)
+    assert L.pcr_pipeline_run(lay2, 2, P(bat2), 0, 0x5, 0x6, None) == pcr.PCR_ERR_INVALID_ARG
+    assert "pcr_pipeline_run" in pcr.last_error() and "sm_scale" in pcr.last_error()
+    bat2.sm_scale = 0.125
+    lay2[1].q = 18                     # misaligned q in the second layer
+    assert L.pcr_pipeline_run(lay2, 2, P(bat2), 0, 0x5, 0x6, None) == pcr.PCR_ERR_INVALID_ARG
+    assert "aligned" in pcr.last_error()
+    lay2[1].q = 16
+    bat2.num_q_heads = 3
+    assert L.pcr_pipeline_run_offload(lay2, None, 2, P(bat2), None, None, 0, 0, 0, None, 0, 0x5, 0x6, 0x7,
+                                      None) == pcr.PCR_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("mk", [synth.tiny, synth.l8b_layer, synth.l70b_pipe80])
