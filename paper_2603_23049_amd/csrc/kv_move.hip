@@ -35,6 +35,17 @@ __global__ __launch_bounds__(256) void append_kv_kernel(
     const int tile = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
     const int tok0 = tile * kTileTokens;
 
+    // The K/V rows do not depend on the slot list: their loads go out first, so the two
+    // memory round trips (slots, rows) overlap.
+    const int r = tid / CPR, c = tid % CPR;
+    const bool mine = tid < kTileTokens * CPR && tok0 + r < T;
+    u32x4 kv{}, vv{};
+    if (mine) {
+        const int64_t src = ((int64_t)(tok0 + r) * Hkv + g) * D + c * 8;
+        kv = *reinterpret_cast<const u32x4 *>(k_new + src);
+        vv = *reinterpret_cast<const u32x4 *>(v_new + src);
+    }
+
     if (tid < kTileTokens) {
         const int t = tok0 + tid;
         int32_t sl = -1;
@@ -46,20 +57,13 @@ __global__ __launch_bounds__(256) void append_kv_kernel(
     }
     __syncthreads();
 
-    if (tid < kTileTokens * CPR) {
-        const int r = tid / CPR, c = tid % CPR;
-        const int t = tok0 + r;
-        if (t < T) {
-            const int64_t src = ((int64_t)t * Hkv + g) * D + c * 8;
-            const u32x4 kv = *reinterpret_cast<const u32x4 *>(k_new + src);
-            const u32x4 vv = *reinterpret_cast<const u32x4 *>(v_new + src);
-            *reinterpret_cast<u32x4 *>(&vs[r][c * 8]) = vv;
-            const int32_t sl = slots[r];
-            if (sl >= 0) {
-                const int64_t blk = sl / kBlockSize, o = sl % kBlockSize;
-                const int64_t dst = ((blk * Hkv + g) * kBlockSize + o) * D + c * 8;
-                *reinterpret_cast<u32x4 *>(pool_k + dst) = kv;
-            }
+    if (mine) {
+        *reinterpret_cast<u32x4 *>(&vs[r][c * 8]) = vv;
+        const int32_t sl = slots[r];
+        if (sl >= 0) {
+            const int64_t blk = sl / kBlockSize, o = sl % kBlockSize;
+            const int64_t dst = ((blk * Hkv + g) * kBlockSize + o) * D + c * 8;
+            *reinterpret_cast<u32x4 *>(pool_k + dst) = kv;
         }
     }
     __syncthreads();
