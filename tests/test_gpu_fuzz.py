@@ -4,7 +4,9 @@ Each case draws a ragged batch (1-10 sequences; prefix and suffix lengths half f
 block, tile and row-tile edges, half uniform; G from 1 to 16 query heads per kv head;
 head_dim 64 or 128), runs the serial layer (load, append, prefill attention) and
 checks every row, then runs the decode entry point on each sequence's last token over
-the same pool and checks it against the same oracle rows."""
+the same pool and checks it against the same oracle rows. The copy cases draw batches
+the same way and check the plans, the pool after load and append, a gather and an
+offload bit for bit."""
 import numpy as np
 import pytest
 import torch
