@@ -328,9 +328,11 @@ typedef struct pcr_batch {
 
 /*
  * pcr_pipeline_run -- the layer-wise overlapped step (Sec. 4.3; Alg. 1
- * "LayerwiseUpload" and "WaitForUploadEvents"). Every layer's load is enqueued
- * up front on copy_stream, each followed by an event; compute_stream waits on
- * layer l's event, then runs layer l's append and attention. Layers are
+ * "LayerwiseUpload" and "WaitForUploadEvents"). Every layer's load goes on
+ * copy_stream, each followed by an event; compute_stream waits on layer l's
+ * event, then runs layer l's append and attention. The host queues layer by
+ * layer (load l, then compute l), so the copy stream runs the loads back to back
+ * while the compute stream starts as soon as the first load is done. Layers are
  * independent here (each layer's Q and new K/V are inputs).
  * timing_ms: NULL, or host float[4*n_layers + 2]. When given, the call waits for
  * the last layer and fills, per layer l: [4l] load ms, [4l+1] compute ms
