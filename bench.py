@@ -197,8 +197,9 @@ class ClockSampler:
             return
         script = (f"read go || exit 0; for i in $(seq 1 {n}); do echo @sample; "
                   f"timeout 5 {smi} metric -g 0 --clock --power --json 2>/dev/null; sleep {period_s}; done")
+        # its own process group, so that close() can end the shell and any amd-smi child
         self.proc = subprocess.Popen(["bash", "-c", script], stdin=subprocess.PIPE, stdout=subprocess.PIPE,
-                                     stderr=subprocess.DEVNULL, text=True)
+                                     stderr=subprocess.DEVNULL, text=True, start_new_session=True)
 
     def start(self):
         if self.proc:
@@ -208,6 +209,13 @@ class ClockSampler:
     def running(self):
         return self.proc is not None and self.proc.poll() is None
 
+    def _kill_group(self):
+        import signal
+        try:
+            os.killpg(self.proc.pid, signal.SIGKILL)
+        except (ProcessLookupError, PermissionError):
+            pass
+
     def collect(self, timeout=30):
         """[(gfx MHz per XCD, socket power W)] of the samples that parsed."""
         if self.proc is None:
@@ -215,7 +223,8 @@ class ClockSampler:
         try:
             out, _ = self.proc.communicate(timeout=timeout)
         except Exception:
-            self.proc.kill()
+            self._kill_group()
+            self.proc.wait()
             return []
         samples = []
         for body in out.split("@sample")[1:]:
@@ -229,12 +238,21 @@ class ClockSampler:
         return samples
 
     def close(self):
-        if self.proc and self.proc.poll() is None:
+        """Ends the sampling shell and everything it started (its whole process group),
+        and reaps it, so no process outlives the benchmark."""
+        if self.proc is None:
+            return
+        if self.proc.poll() is None:
             try:
                 self.proc.stdin.close()
                 self.proc.wait(timeout=10)
             except Exception:
-                self.proc.kill()
+                pass
+        self._kill_group()       # a hung amd-smi child may outlive the shell
+        try:
+            self.proc.wait(timeout=10)
+        except Exception:
+            pass
 
 
 def measure_clock_hold(batch, sampler, settle_s=0.5, max_s=15.0):

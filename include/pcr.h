@@ -345,9 +345,15 @@ typedef struct pcr_batch {
  * queue run in series. Create these streams before others, or raise
  * GPU_MAX_HW_QUEUES before HIP starts (the same holds for the three streams of
  * pcr_pipeline_run_offload).
- * Errors: the attention arguments of every layer (batch-wide lengths, heads,
- * sm_scale, block table size; each layer's pool, q and out) are checked before
- * anything is queued, and an error there leaves the streams untouched. A later
+ * Every layer must have its own pool: nothing orders a later layer's load (copy
+ * stream) after an earlier layer's attention (compute stream), so layers sharing
+ * pool memory would race. Pool K/V base pointers repeated across layers (or a
+ * layer's K equal to its V) are refused with PCR_ERR_INVALID_ARG; pools that
+ * overlap at different base addresses are not detected and are the caller's error.
+ * Errors: the pools' distinctness and the attention arguments of every layer
+ * (batch-wide lengths, heads, sm_scale, block table size; each layer's pool, q
+ * and out) are checked before anything is queued, and an error there leaves the
+ * streams untouched. A later
  * error (a load's block list or unpinned host memory, found when that layer's
  * load is queued; a failed launch) returns with the earlier layers' work still
  * queued: it runs to completion, and the pools' contents are then unspecified.
@@ -391,9 +397,11 @@ pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_k
  * page-aligned buffers (e.g. pinned host memory) with a page-multiple chunk size
  * bypass the page cache (O_DIRECT). No GPU work is involved.
  *   pcr_store_write_async   queue chunk_bytes from src as chunk chunk_id
- *   pcr_store_read_async    queue a read of chunk chunk_id into dst; first waits for
- *                           earlier writes of that chunk; PCR_ERR_INVALID_ARG if the
- *                           chunk was never written
+ *   pcr_store_read_async    queue a read of chunk chunk_id into dst; PCR_ERR_INVALID_ARG
+ *                           if the chunk was never written
+ * Tasks of one chunk run one at a time, in submission order: both submit calls
+ * first block until the chunk's earlier tasks are done (tasks of other chunks run
+ * concurrently on the I/O threads).
  *   pcr_store_wait          block until chunk_id's tasks (or, for chunk_id < 0, all
  *                           tasks) are done; reports the first I/O error, if any
  *   pcr_store_poll          *done = 1 if nothing is pending for chunk_id (or at all)

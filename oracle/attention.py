@@ -35,7 +35,7 @@ def open_library(path):
 def _load():
     global _lib
     if _lib is None:
-        _lib = open_library(_build.ensure_built())
+        _lib = open_library(_build.require_built())
     return _lib
 
 

@@ -161,6 +161,12 @@ int pcr_oracle_attention_rows(const uint16_t *q, int Hq, int Hkv, int d, int bs,
 }
 
 /* Number of threads the OpenMP runtime will use (for reporting). */
+#ifndef PCR_ORACLE_SOURCE_SHA256
+#define PCR_ORACLE_SOURCE_SHA256 "unknown"
+#endif
+/* SHA-256 of the source this library was built from (set by the build script). */
+const char *pcr_oracle_source_sha256(void) { return PCR_ORACLE_SOURCE_SHA256; }
+
 int pcr_oracle_num_threads(void)
 {
     int n = 1;

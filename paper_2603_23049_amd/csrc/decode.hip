@@ -147,7 +147,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
                                                                0, 0, 0);
         }
         const int k0 = kbeg + step * kStepKeys;
-        if (k0 + kStepKeys > kend) {               // wave-uniform: only a chunk's last step is ragged
+        const bool ragged = k0 + kStepKeys > kend;  // wave-uniform: only a chunk's last step is ragged
+        if (ragged) {
 #pragma unroll
             for (int r = 0; r < 2; ++r)
 #pragma unroll
@@ -176,9 +177,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
         }
+        // In a ragged step the V^T operand entries of keys >= kend are cleared: their P is 0,
+        // but the slots past a context's end may hold anything (never written, or another
+        // request's data), and 0 * NaN or 0 * Inf would poison every output column. The
+        // lane's 8 values are keys k0 + 8*q4 .. +7, the same keys as its P^T operand.
+        const int nvalid = kend - (k0 + 8 * q4);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            o[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(R.v[mt]), pb, o[mt], 0, 0, 0);
+        for (int mt = 0; mt < MT; ++mt) {
+            u32x4 vv = R.v[mt];
+            if (ragged) {
+#pragma unroll
+                for (int wd = 0; wd < 4; ++wd)
+                    vv[wd] &= (2 * wd < nvalid ? 0x0000FFFFu : 0u) | (2 * wd + 1 < nvalid ? 0xFFFF0000u : 0u);
+            }
+            o[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[mt], 0, 0, 0);
+        }
     };
 
     if (active) {

@@ -8,6 +8,7 @@
 // then copies the layer's new blocks to the host store. The copy stream first
 // waits for everything already queued on the compute (and offload) stream, so a
 // load never overwrites a pool that earlier work is still reading.
+#include <algorithm>
 #include <vector>
 
 #include "pcr_internal.h"
@@ -69,6 +70,21 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
         if (n_off < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_off < 0", who);
         if (n_off > 0 && (!offload_dst || !off_src || !off_dst))
             return fail(PCR_ERR_INVALID_ARG, "%s: NULL offload argument", who);
+    }
+    // Every layer needs a pool of its own: nothing orders layer l+1's load (copy stream)
+    // after layer l's compute (compute stream), so two layers sharing pool memory would
+    // have one layer's load overwrite blocks the other's attention is still reading.
+    {
+        std::vector<const void *> bufs;
+        bufs.reserve(2 * (size_t)n_layers);
+        for (int32_t l = 0; l < n_layers; ++l) {   // NULL pools are reported by the checks below
+            if (layers[l].pool.k) bufs.push_back(layers[l].pool.k);
+            if (layers[l].pool.v) bufs.push_back(layers[l].pool.v);
+        }
+        std::sort(bufs.begin(), bufs.end());
+        if (std::adjacent_find(bufs.begin(), bufs.end()) != bufs.end())
+            return fail(PCR_ERR_INVALID_ARG, "%s: two layers (or a layer's K and V) share a pool buffer; every "
+                        "layer needs its own pool", who);
     }
     // The attention's arguments, batch-wide and per layer, are checked before anything is
     // queued, so a bad scale, head count or length table leaves the streams untouched.

@@ -7,8 +7,12 @@
 // pool of I/O threads serves a FIFO of read and write tasks with positional I/O
 // (pread/pwrite), opening the file with O_DIRECT when the chunk size and the
 // caller's buffers are page-aligned, so reads measure the device rather than the
-// page cache. Completion is tracked per chunk id: a chunk's read waits for an
-// earlier write of the same chunk to finish.
+// page cache. Completion is tracked per chunk id. Tasks of one chunk run one at a
+// time in submission order: submitting a read or a write of a chunk first waits
+// (in the submitting thread) until every earlier task of that chunk is done, so
+// with several I/O threads a read never sees a half-written chunk and two writes
+// of a chunk land in the order they were submitted. Tasks of different chunks
+// run concurrently.
 #include <errno.h>
 #include <stdio.h>
 #include <fcntl.h>
@@ -111,12 +115,10 @@ pcr_status submit(pcr_chunk_store *st, bool write, int64_t id, void *buf, const 
     if (!buf) return pcr::fail(PCR_ERR_INVALID_ARG, "%s: NULL buffer", who);
     if (id > INT64_MAX / st->chunk_bytes - 1) return pcr::fail(PCR_ERR_INVALID_ARG, "%s: chunk id too large", who);
     std::unique_lock<std::mutex> lk(st->mu);
-    if (!write) {
-        // a read sees the chunk only once it is on the device: wait for earlier writes of it
-        st->cv_done.wait(lk, [&] { return st->pending.find(id) == st->pending.end(); });
-        if (st->written.find(id) == st->written.end())
-            return pcr::fail(PCR_ERR_INVALID_ARG, "%s: chunk %lld was never written", who, (long long)id);
-    }
+    // One task per chunk at a time: wait for the chunk's earlier reads and writes.
+    st->cv_done.wait(lk, [&] { return st->pending.find(id) == st->pending.end(); });
+    if (!write && st->written.find(id) == st->written.end())
+        return pcr::fail(PCR_ERR_INVALID_ARG, "%s: chunk %lld was never written", who, (long long)id);
     st->queue.push_back({write, id, buf});
     ++st->pending[id];
     ++st->total_pending;

@@ -309,7 +309,8 @@ def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, 
                 workspace=None, sm_scale: Optional[float] = None, stream=None):
     """pcr_decode_attn. q/out [B][Hq][d], block_tables [B][max_blocks], context_lens [B] on the
     device; host_context_lens is the host copy. Without a workspace one of the needed size
-    is allocated on q's device."""
+    is allocated on q's device, from the pool of the stream the kernels run on, so that
+    the caching allocator reuses it only after that stream has passed them."""
     hcl = _i32_host(host_context_lens)
     B = int(hcl.shape[0])
     if sm_scale is None:
@@ -317,7 +318,15 @@ def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, 
     if workspace is None and B > 0:
         import torch
         n = decode_attn_workspace_bytes(B, num_q_heads, pool.num_kv_heads, pool.head_dim, int(hcl.max()))
-        workspace = torch.empty(n, dtype=torch.uint8, device=q.device) if n > 0 else None
+        if n > 0:
+            if stream is None:
+                s = torch.cuda.current_stream(q.device)
+            elif isinstance(stream, int):
+                s = torch.cuda.ExternalStream(stream, device=q.device)
+            else:
+                s = stream
+            with torch.cuda.stream(s):
+                workspace = torch.empty(n, dtype=torch.uint8, device=q.device)
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
     p = pool.c()
     _check(lib().pcr_decode_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),

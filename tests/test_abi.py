@@ -154,7 +154,7 @@ def test_argument_validation_before_any_device_work():
     # (the stream handles are never used on these paths)
     lay2 = (pcr._LayerIO * 2)()
     for i in range(2):
-        lay2[i].pool = _pool(Hkv=2)
+        lay2[i].pool = _pool(Hkv=2, k=0x10000 + 0x100000 * i, v=0x20000 + 0x100000 * i)
         lay2[i].q = lay2[i].out = 16
     bat2 = pcr._Batch(block_tables=16, max_blocks=4, prefix_lens=16, cu_suffix=16,
                       host_prefix_lens=hpl.ctypes.data, host_cu_suffix=hcu.ctypes.data, B=1, num_q_heads=4,
@@ -166,6 +166,15 @@ def test_argument_validation_before_any_device_work():
     assert L.pcr_pipeline_run(lay2, 2, P(bat2), 0, 0x5, 0x6, None) == pcr.PCR_ERR_INVALID_ARG
     assert "aligned" in pcr.last_error()
     lay2[1].q = 16
+    # two layers on one pool (or a pool whose K is its V) are refused before anything is queued
+    lay2[1].pool = _pool(Hkv=2)
+    lay2[0].pool = _pool(Hkv=2)
+    assert L.pcr_pipeline_run(lay2, 2, P(bat2), 0, 0x5, 0x6, None) == pcr.PCR_ERR_INVALID_ARG
+    assert "own pool" in pcr.last_error()
+    lay2[1].pool = _pool(Hkv=2, k=0x50000, v=0x50000)
+    lay2[0].pool = _pool(Hkv=2)
+    assert L.pcr_pipeline_run(lay2, 2, P(bat2), 0, 0x5, 0x6, None) == pcr.PCR_ERR_INVALID_ARG
+    lay2[1].pool = _pool(Hkv=2, k=0x110000, v=0x120000)
     bat2.num_q_heads = 3
     assert L.pcr_pipeline_run_offload(lay2, None, 2, P(bat2), None, None, 0, 0, 0, None, 0, 0x5, 0x6, 0x7,
                                       None) == pcr.PCR_ERR_UNSUPPORTED

@@ -94,6 +94,46 @@ def test_decode_ragged_merged_in_workgroup(B, d):
     _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode merged B={B} d={d}")
 
 
+NAN_BITS = np.uint16(0x7FC1)
+
+
+def _poison_past_end(pk, pv, bt, ctx):
+    """NaN bit patterns in every slot of each sequence's last block past its context end
+    (K and V): the slots a ragged step reads but must not use."""
+    pk, pv = pk.copy(), pv.copy()
+    for i, n in enumerate(ctx):
+        if n % BS:
+            blk = int(bt[i, (n - 1) // BS])
+            pk[blk, :, (n % BS) * pk.shape[2] // BS:] = NAN_BITS   # K: slot-major rows of d
+            vb = pv[blk].reshape(pv.shape[1], -1, BS)               # V: d-major rows of 16 slots
+            vb[:, :, n % BS:] = NAN_BITS
+    return pk, pv
+
+
+@pytest.mark.parametrize("regime,B", [("one_chunk", 160), ("lds_merge", 40), ("workspace", 3)])
+def test_decode_nan_past_context_end(regime, B):
+    """Pool slots past each context end hold NaN bit patterns (never-written slots, or
+    another request's garbage): the output stays finite and equal to the oracle, which
+    never reads them. Contexts are not multiples of 16 and end in either block of the
+    last 32-key step, for single-chunk sequences, chunks merged in the workgroup and
+    chunks merged through the workspace."""
+    Hq, Hkv, d = 32, 8, 128
+    rng = np.random.Generator(np.random.PCG64(1000 + B))
+    hi = {"one_chunk": 250, "lds_merge": 4000, "workspace": 40000}[regime]
+    ctx = [int(x) for x in rng.integers(1, hi, B)]
+    ctx = [n + 1 if n % BS == 0 else n for n in ctx]
+    ctx[0] = 17 if regime == "one_chunk" else hi - 7
+    ctx[1] = 9
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=2000 + B)
+    pk, pv = _poison_past_end(pk, pv, bt, ctx)
+    ws = pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, max(ctx))
+    assert (ws > 0) == (regime == "workspace")
+    say(f"[gpu] decode NaN past context end: {regime} B={B} max_ctx={max(ctx)} workspace={ws}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode NaN tail {regime}")
+
+
 def test_decode_long_contexts():
     """Contexts of 131072 and 65537 keys (two sequences): 64 and 33 chunks of 2048 keys
     merged through the workspace (the last one holding a single key), fp32 sums over

@@ -58,3 +58,31 @@ def test_window_prefetch_serves_correct_bytes_and_cuts_on_demand_reads(scratch):
     assert s4.prefetch_hits > 0
     assert s4.on_demand_reads < s0.on_demand_reads
     assert s0.hit_tokens == s4.hit_tokens > 0     # the tiers change when bytes move, not what hits
+
+
+def test_store_tasks_of_one_chunk_run_in_submission_order(scratch):
+    """Writes, reads and writes of one chunk interleaved, with four I/O threads and
+    other chunks' tasks in between: every read returns the write submitted just before
+    it (never a torn mix), and the chunk ends with the last write."""
+    cb = 256 * 1024
+    st = pcr.ChunkStore(os.path.join(scratch, "order.bin"), cb, io_threads=4)
+    versions = [np.full(cb, v, np.uint8) for v in range(1, 13)]
+    others = [prefetch.chunk_pattern(50 + i, cb) for i in range(12)]
+    reads = [np.zeros(cb, np.uint8) for _ in versions]
+    for i, (w, o) in enumerate(zip(versions, others)):
+        st.write_async(0, w)
+        st.write_async(1 + i, o)
+        st.read_async(0, reads[i])
+    st.wait()
+    for i, r in enumerate(reads):
+        assert np.all(r == i + 1), f"read {i} saw a different or torn version"
+    final = np.zeros(cb, np.uint8)
+    st.read_async(0, final)
+    st.wait()
+    assert np.all(final == len(versions))
+    back = [np.zeros(cb, np.uint8) for _ in others]
+    for i, b in enumerate(back):
+        st.read_async(1 + i, b)
+    st.wait()
+    assert all(np.array_equal(b, o) for b, o in zip(back, others))
+    st.close()
