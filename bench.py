@@ -48,7 +48,9 @@ if ROOT not in sys.path:
 MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16
 HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
 ATTN_SOURCE = os.path.join(ROOT, "paper_2603_23049_amd", "csrc", "attn.hip")
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "prefill_attn_l8b_layer_traffic.md")
+# Committed counter summaries of the attention's HBM traffic, per workload.
+TRAFFIC_PROFILES = {"l70b_pipe80": os.path.join(ROOT, "profiles", "prefill_attn_l70b_pipe80_layer_traffic.md"),
+                    "l8b_layer": os.path.join(ROOT, "profiles", "prefill_attn_l8b_layer_traffic.md")}
 
 
 def source_sha256(path: str) -> str:
@@ -57,13 +59,15 @@ def source_sha256(path: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per attention launch from the committed counter summary, or None when
-    the summary is missing or was taken on a different attention source."""
-    if not os.path.exists(TRAFFIC_PROFILE):
+def measured_traffic(workload_name: str):
+    """HBM bytes per attention launch from the committed counter summary of this
+    workload, or None when the summary is missing or was taken on a different
+    attention source."""
+    path = TRAFFIC_PROFILES.get(workload_name)
+    if path is None or not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_PROFILE):
+    for line in open(path):
         if line.startswith("- ") and ":" in line:
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
@@ -130,10 +134,10 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _setup_layer(batch, layer=0, method="kernel_pull"):
+def _setup_layer(batch, layer=0, method="kernel_pull", data=None):
     import torch
     from paper_2603_23049_amd import pcr, synth
-    data = synth.make_layer(batch, layer)
+    data = synth.make_layer(batch, layer) if data is None else data
     Hkv, d, bs = batch.num_kv_heads, batch.head_dim, batch.block_size
 
     def dev(a):
@@ -158,19 +162,23 @@ def _setup_layer(batch, layer=0, method="kernel_pull"):
 
 def _setup_pipeline(batch, distinct):
     """n layers with their own pools; host store, Q and new K/V come from `distinct`
-    generated layers used round-robin (same bytes moved and computed per layer)."""
+    generated data sets, layer l taking set l % distinct (the same bytes are moved and
+    computed per layer either way; the GPU tests run the same assignment)."""
     import torch
-    from paper_2603_23049_amd import pcr
+    from paper_2603_23049_amd import pcr, synth
+    sets = synth.pipeline_data_sets(batch.num_layers, distinct)
+    datas = synth.make_layers(batch, range(max(sets) + 1))
     base = []
     bp = None
-    for l in range(min(distinct, batch.num_layers)):
-        L, bp_l, _ = _setup_layer(batch, l)
+    for k, data in enumerate(datas):
+        L, bp_l, _ = _setup_layer(batch, k, data=data)
         base.append(L)
         bp = bp or bp_l
+    del datas
     layers = list(base)
     Hkv, d, bs = batch.num_kv_heads, batch.head_dim, batch.block_size
     for l in range(len(base), batch.num_layers):
-        src = base[l % len(base)]
+        src = base[sets[l]]
         pool = pcr.KVPool(torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"),
                           torch.zeros((batch.pool_blocks, Hkv, bs * d), dtype=torch.int16, device="cuda"), Hkv, d)
         layers.append(pcr.Layer(src.host, pool, src.q, src.k_new, src.v_new, src.out))
@@ -312,52 +320,58 @@ def warm_up(fn, min_ms, min_calls=3):
                 return n
 
 
-def measure_step(batch, steps, warmup, min_warm_ms=0.0):
-    """Timed compute step (append + attention) with prefix KV already in the pool: one
-    event pair and the wall clock around all `steps` steps, synchronized on both sides
-    (an event pair per step would put its own gaps between the steps: about 7 us per
-    step measured), after `warmup` steps and, with min_warm_ms, at least that much
-    warm-up time. Then the attention and append kernels alone, back to back, for their
-    per-launch time."""
+def measure_step(batch, steps, warmup, min_warm_ms=500.0):
+    """Timed compute step (append + attention) with prefix KV already in the pool.
+
+    Warm-up: `warmup` steps, then more until at least min_warm_ms of sustained work has
+    passed (after an idle gap the GPU clock starts low and ramps up under load), whatever
+    `warmup` says. Timed region: `steps` steps between one event pair and the wall clock,
+    synchronized on both sides; inside it each attention launch is bracketed by its own
+    event pair on the stream it runs on, so the attention's per-launch time comes from
+    the same window as the step time. Then the append alone, back to back, for its
+    per-launch time (a launch-bound kernel at these sizes)."""
     import torch
     from paper_2603_23049_amd import pcr
     L, bp, _ = _setup_layer(batch)
     pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="kernel_pull")
     torch.cuda.synchronize()
     s = torch.cuda.current_stream()
+
     def step():
         pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
         _attn(L, bp, s)
 
     for _ in range(warmup):
         step()
-    if min_warm_ms > 0:
-        warm_up(step, min_warm_ms)
+    warm_calls = warm_up(step, min_warm_ms)
     torch.cuda.synchronize()
-    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a, e = ev(), ev()
+    pairs = [(ev(), ev()) for _ in range(steps)]
     t0 = time.perf_counter()
     a.record(s)
-    for _ in range(steps):
+    for x, y in pairs:
         pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
+        x.record(s)
         _attn(L, bp, s)
+        y.record(s)
     e.record(s)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     step_ms = a.elapsed_time(e) / steps
+    launches = [x.elapsed_time(y) for x, y in pairs]
+    attn_ms = float(np.mean(launches))
 
-    def back_to_back(fn):
-        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(s)
-        for _ in range(steps):
-            fn()
-        e.record(s)
-        e.synchronize()
-        return a.elapsed_time(e) / steps
-
-    attn_ms = back_to_back(lambda: _attn(L, bp, s))
-    append_ms = back_to_back(lambda: pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s))
+    a2, e2 = ev(), ev()
+    a2.record(s)
+    for _ in range(steps):
+        pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping, stream=s)
+    e2.record(s)
+    e2.synchronize()
+    append_ms = a2.elapsed_time(e2) / steps
     return dict(step_ms=float(step_ms), wall_ms_per_step=wall / steps * 1e3, append_ms=append_ms,
-                attn_ms=attn_ms, wall_s=wall)
+                attn_ms=attn_ms, attn_ms_min=float(min(launches)), attn_ms_max=float(max(launches)),
+                attn_ms_median=_median(launches), wall_s=wall, warmup_calls=warmup + warm_calls)
 
 
 def measure_load(batch, reps=10):
@@ -637,71 +651,231 @@ def measure_pipeline_offload(batch, method, load_ms_iso, compute_ms_iso, offload
             "synchronous_ms": n * (load_ms_iso + compute_ms_iso + offload_ms_iso)}
 
 
-def cpu_baseline(batch, budget_s=12.0):
-    """The fp64 oracle (as it stands) on the same layer, repeated until about budget_s
-    of CPU time has passed; TFLOP/s by the layer's causal-exact FLOPs."""
-    from oracle import attention as oattn
+def _oracle_layer(batch, layer=0):
+    """One layer's oracle inputs: the layer's data, the plan, and the pools after the
+    oracle's own load and append."""
     from oracle import datamove as odm
     from paper_2603_23049_amd import synth
-    data = synth.make_layer(batch, 0)
+    data = synth.make_layer(batch, layer)
     plan = odm.plan(batch.prefix_lens, batch.suffix_lens, batch.block_tables, batch.host_blocks, 16)
     shape = (batch.pool_blocks, batch.num_kv_heads, 16 * batch.head_dim)
     pk, pv = odm.pool_after_layer(np.zeros(shape, np.uint16), np.zeros(shape, np.uint16), data.host_k, data.host_v,
                                   plan, data.k_new, data.v_new)
-    flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
+    return data, plan, pk, pv
+
+
+def _time_oracle_attention(batch, budget_s=0.0, rows=None, inputs=None):
+    """The fp64 oracle on a layer (every row, or the given (token, head) rows), repeated
+    until budget_s of wall time has passed (at least once). Returns (passes, seconds,
+    FLOPs per pass)."""
+    from oracle import attention as oattn
+    data, plan, pk, pv = inputs or _oracle_layer(batch)
+    pl = np.asarray(batch.prefix_lens, np.int32)
+    if rows is None:
+        flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
+    else:   # 4*d FLOPs per (row, visible key) pair
+        cu = plan[3]
+        seq = np.searchsorted(cu, rows[:, 0], side="right") - 1
+        keys = pl[seq] + (rows[:, 0] - cu[seq]) + 1
+        flops = 4.0 * batch.head_dim * float(keys.sum())
     reps, t0 = 0, time.perf_counter()
     while True:
-        oattn.attention(data.q, pk, pv, batch.block_tables, np.asarray(batch.prefix_lens, np.int32), plan[3],
-                        batch.num_kv_heads, 16)
+        oattn.attention(data.q, pk, pv, batch.block_tables, pl, plan[3], batch.num_kv_heads, 16, rows=rows)
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= budget_s:
-            break
+            return reps, dt, flops
+
+
+def cpu_baseline(batch, budget_s=12.0, inputs=None):
+    """The fp64 oracle (as it stands) on one whole layer of the headline workload (every
+    row of every head), repeated until about budget_s has passed; TFLOP/s by the layer's
+    causal-exact FLOPs."""
+    from oracle import attention as oattn
+    reps, dt, flops = _time_oracle_attention(batch, budget_s, inputs=inputs)
     return {"value": reps * flops / dt / 1e12, "unit": "TFLOP/s", "cores": oattn.num_threads(), "kind": "oracle",
-            "sample": f"the whole {batch.name} layer (every row of every head), fp64, {reps} passes in {dt:.1f} s"}
+            "sample": f"one whole layer of {batch.name} (every row of every head), fp64, {reps} pass(es) in "
+                      f"{dt:.1f} s", "ms_per_layer": dt / reps * 1e3}
+
+
+def cpu_baseline_legs(headline=None):
+    """The oracle timed on the other configurations (reported beside the headline, never
+    a target): tiny, the Llama-3-8B layer and the RAG mix in full; one layer of the
+    32-layer stack (the 8B layer's shape) and of the 80-layer stack with the x n
+    extrapolation labelled; one thread on a sampled part of the 8B layer; and the host
+    memcpy rates of the load, append and gather oracles."""
+    from oracle import attention as oattn
+    from oracle import datamove as odm
+    from paper_2603_23049_amd import synth
+    cores = oattn.num_threads()
+    legs = {"cores": cores}
+    for name in ("tiny", "l8b_layer", "rag_mix"):
+        b = workload(name)
+        reps, dt, flops = _time_oracle_attention(b, 1.0)
+        legs[name] = {"ms": dt / reps * 1e3, "GFLOPs": flops / dt * reps / 1e9, "flops": flops,
+                      "what": f"every row of every head, {reps} pass(es)"}
+    per = legs["l8b_layer"]["ms"]
+    legs["l8b_pipe32"] = {"ms_per_layer": per, "ms_extrapolated_x32": 32 * per,
+                          "what": "one layer timed (the l8b_layer shape), x32 extrapolated"}
+    if headline is not None:
+        legs["l70b_pipe80"] = {"ms_per_layer": headline["ms_per_layer"],
+                               "ms_extrapolated_x80": 80 * headline["ms_per_layer"],
+                               "what": "one layer timed (the headline cpu_baseline), x80 extrapolated"}
+    # one thread: every 8th token's rows of the 8B layer
+    b = synth.l8b_layer()
+    inputs = _oracle_layer(b)
+    rows = np.array([[t, h] for t in range(0, b.T, 8) for h in range(b.num_q_heads)], np.int32)
+    oattn.set_num_threads(1)
+    try:
+        reps, dt, flops = _time_oracle_attention(b, 3.0, rows=rows, inputs=inputs)
+    finally:
+        oattn.set_num_threads(cores)
+    legs["one_thread"] = {"GFLOPs": reps * flops / dt / 1e9, "threads": 1,
+                          "what": f"l8b_layer, every 8th new token's rows ({len(rows)} rows), {reps} pass(es)"}
+    # host memcpy rates of the bit-copy oracles on the 8B layer
+    data, plan, pk, pv = inputs
+    src, dst, slots, cu = plan
+    zk, zv = np.zeros_like(pk), np.zeros_like(pv)
+    t0 = time.perf_counter()
+    odm.load(zk, zv, data.host_k, data.host_v, src, dst)
+    t_load = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    odm.append(zk, zv, data.k_new, data.v_new, slots, 16)
+    t_app = time.perf_counter() - t0
+    starts = np.zeros(b.B, np.int64)
+    lens = [512] * b.B                   # the first 512 tokens of each sequence
+    t0 = time.perf_counter()
+    odm.gather(pk, pv, b.block_tables, starts, lens, b.head_dim, 16)
+    t_gat = time.perf_counter() - t0
+    lb = load_bytes(b.prefix_lens, b.num_kv_heads, b.head_dim)
+    ab = append_bytes(b.T, b.num_kv_heads, b.head_dim)
+    gb = 2 * sum(lens) * b.num_kv_heads * b.head_dim * 2 * 2
+    legs["memcpy"] = {"load_GBps": lb / t_load / 1e9, "append_GBps": ab / t_app / 1e9,
+                      "gather_GBps": gb / t_gat / 1e9,
+                      "what": "numpy bit-copy oracles on the l8b_layer layer (load 64 MiB, append 4+4 MiB, "
+                              "gather of each sequence's first 512 tokens; bytes read + written)"}
+    return legs
+
+
+def hit_ratio_report(capacities=(64, 128, 200, 300), n_requests=400):
+    """RAG-mix stream (seed 4, 400 requests): token hit ratio through a prefix tree of
+    limited capacity (in 256-token chunks), with the look-ahead over the next 4 waiting
+    requests and with plain leaf LRU; and with no capacity limit."""
+    from paper_2603_23049_amd import prefix_tree as pt
+    out = {"stream": f"rag_stream(4), {n_requests} requests, first 64 only warm the tree", "window": 4}
+    rows = []
+    for cap in capacities:
+        rows.append({"capacity_chunks": cap,
+                     "lookahead": pt.hit_ratio_under_capacity(4, capacity_chunks=cap, lookahead=True,
+                                                              n_requests=n_requests),
+                     "lru": pt.hit_ratio_under_capacity(4, capacity_chunks=cap, lookahead=False,
+                                                        n_requests=n_requests)})
+    out["by_capacity"] = rows
+    out["unbounded"] = pt.hit_ratio_under_capacity(4, capacity_chunks=None, lookahead=False, n_requests=n_requests)
+    return out
+
+
+def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8, d=128, reps=20):
+    """The scatter (pcr_append_kv) from 1k to 128k new tokens (8 MiB to 1 GiB of K+V
+    moved: every row read once and written once), each size timed back to back after a
+    warm-up; the pool holds exactly the tokens' blocks in a random order."""
+    import torch
+    from paper_2603_23049_amd import pcr
+    bs = 16
+    s = torch.cuda.current_stream()
+    out = []
+    g = torch.Generator(device="cuda").manual_seed(17)
+    for T in token_counts:
+        nb = -(-T // bs)
+        pool = pcr.KVPool(torch.zeros((nb, Hkv, bs * d), dtype=torch.int16, device="cuda"),
+                          torch.zeros((nb, Hkv, bs * d), dtype=torch.int16, device="cuda"), Hkv, d)
+        k = torch.randint(-32768, 32767, (T, Hkv, d), dtype=torch.int16, device="cuda", generator=g)
+        v = torch.randint(-32768, 32767, (T, Hkv, d), dtype=torch.int16, device="cuda", generator=g)
+        perm = torch.randperm(nb, device="cuda", generator=g).to(torch.int32)
+        slots = (perm.repeat_interleave(bs)[:T] * bs + torch.arange(T, device="cuda", dtype=torch.int32) % bs)
+        slots = slots.to(torch.int32).contiguous()
+        fn = lambda: pcr.append_kv(pool, k, v, slots, stream=s)
+        warm_up(fn, 30.0)
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(reps):
+            fn()
+        e.record(s)
+        e.synchronize()
+        ms = a.elapsed_time(e) / reps
+        nbytes = append_bytes(T, Hkv, d)
+        out.append({"T": T, "bytes": nbytes, "ms": ms, "GBps": nbytes / ms / 1e6,
+                    "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS})
+        del pool, k, v, slots, perm
+    torch.cuda.synchronize()
+    return {"sizes": out, "asymptotic_GBps": out[-1]["GBps"], "asymptotic_frac_hbm": out[-1]["frac_hbm"]}
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=400,
-                    help="untimed steps first; the GPU clock needs about 200 l8b_layer steps (15 ms) "
-                         "of sustained load to settle")
-    ap.add_argument("--workload", default="l8b_layer")
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20,
+                    help="untimed steps first; the warm-up then continues until at least 500 ms of sustained "
+                         "work has passed (the GPU clock needs that long to settle), whatever this says")
+    ap.add_argument("--workload", default="l70b_pipe80",
+                    help="headline step: one layer (append + attention) of this workload")
+    ap.add_argument("--step-only", action="store_true",
+                    help="only the headline step (the run the kernel-trace and counter profiles take)")
     ap.add_argument("--no-pipeline", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-load", action="store_true", help="skip the host-to-pool copy measurements")
     ap.add_argument("--no-extra", action="store_true",
-                    help="skip the RAG-mix attention line and the 80-layer and compute-bound pipelines")
+                    help="skip the secondary lines (8B layer, RAG mix, decode, SSD tier, offload, append sweep, "
+                         "hit ratios) and the 80-layer and compute-bound pipelines")
     ap.add_argument("--pipeline-method", default="auto")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
     ap.add_argument("--decode-only", action="store_true",
                     help="only run the decode-step measurement and print its JSON")
+    ap.add_argument("--append-sweep-only", action="store_true",
+                    help="only run the append (scatter) sweep and print its JSON")
     ap.add_argument("--pipeline-only", action="store_true",
                     help="only run the 32-layer pipeline (with its isolated load and compute times) and print "
                          "its JSON")
     ap.add_argument("--no-clocks", action="store_true",
                     help="skip the amd-smi clock samples under the attention (never taken under a profiler)")
     args = ap.parse_args(argv)
+    if args.step_only:
+        args.no_pipeline = args.no_cpu_baseline = args.no_load = args.no_extra = args.no_clocks = True
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this path has no cross-GPU exchange and every box here "
               "has one GPU; run with --gpus 1", file=sys.stderr)
         return 2
 
+    # The oracle's library must be current before the GPU is initialised: building it
+    # starts the compiler, which a process that has touched the GPU may not do.
+    if not args.no_cpu_baseline and not (args.copy_calibration or args.decode_only or args.pipeline_only
+                                         or args.append_sweep_only):
+        from oracle import build as obuild
+        obuild.ensure_built()
     # Under a profiler the tool library has initialised the GPU before this script runs,
     # so no other program may be started from here: no clock sampling then.
     under_profiler = (any(k.startswith(("ROCPROF", "ROCP_")) for k in os.environ)
                       or "rocprof" in os.environ.get("LD_PRELOAD", ""))
     sampler = (ClockSampler() if not (args.copy_calibration or args.decode_only or args.pipeline_only or args.no_clocks
-                                      or under_profiler) else None)
+                                      or args.append_sweep_only or under_profiler) else None)
     try:
         return _main(args, sampler)
     finally:
         if sampler:
             sampler.close()
+
+
+def _step_record(batch, st):
+    flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
+    return {"workload": batch.name, "ms_per_step": st["step_ms"], "attn_ms": st["attn_ms"],
+            "attn_ms_median": st["attn_ms_median"], "append_ms": st["append_ms"], "flops": flops,
+            "step_tflops": flops / (st["step_ms"] * 1e-3) / 1e12,
+            "attn_tflops": flops / (st["attn_ms"] * 1e-3) / 1e12,
+            "attn_frac": flops / (st["attn_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "warmup_calls": st["warmup_calls"]}
 
 
 def _main(args, sampler):
@@ -717,6 +891,9 @@ def _main(args, sampler):
     if args.decode_only:
         print(json.dumps({"decode": measure_decode()}), flush=True)
         return 0
+    if args.append_sweep_only:
+        print(json.dumps({"append_sweep": measure_append_sweep()}), flush=True)
+        return 0
     if args.pipeline_only:
         pb = synth.l8b_pipe32()
         pst = measure_step(pb, args.steps, args.warmup)
@@ -728,30 +905,55 @@ def _main(args, sampler):
 
     batch = workload(args.workload)
     flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
-    _say(f"[bench] step: {args.workload} warmup={args.warmup} steps={args.steps}")
+    _say(f"[bench] step: {args.workload} warmup={args.warmup} (+ at least 500 ms) steps={args.steps}")
     st = measure_step(batch, args.steps, args.warmup)
     value = flops / (st["step_ms"] * 1e-3) / 1e12
     attn_tflops = flops / (st["attn_ms"] * 1e-3) / 1e12
     app_b = append_bytes(batch.T, batch.num_kv_heads, batch.head_dim)
     _say(f"[bench] step {st['step_ms']:.4f} ms, attention {st['attn_ms']:.4f} ms = {attn_tflops:.1f} TFLOP/s")
-    _say("[bench] clocks under the attention (amd-smi)")
-    clocks = measure_clock_hold(batch, sampler)
+    clocks = None
+    if sampler is not None:
+        _say("[bench] clocks under the attention (amd-smi)")
+        clocks = measure_clock_hold(batch, sampler)
 
+    method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
     load = None
     if not args.no_load:
         _say("[bench] load")
         load = measure_load(batch)
-    pipe = None
     pipelines = {}
-    method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
+    extra = {}
+    if not args.no_extra:
+        b8 = synth.l8b_layer()
+        _say("[bench] secondary step: l8b_layer")
+        extra["l8b_layer"] = _step_record(b8, measure_step(b8, args.steps, args.warmup, min_warm_ms=300.0))
     if not args.no_pipeline:
         if load is None:
             load = measure_load(batch)
-        pbatch = synth.l8b_pipe32()
-        _say(f"[bench] pipeline: {pbatch.name} ({pbatch.num_layers} layers)")
-        pipe = measure_pipeline(pbatch, args.pipeline_method, load[method]["ms"], st["step_ms"])
-        pipelines[pbatch.name] = pipe
-    extra = {}
+        todo = [(batch, st, load, synth.pipeline_data_sets(batch.num_layers, 6))]
+        if not args.no_extra:
+            for pb in (synth.l8b_pipe32(), synth.l8b_pipe32(suffix=6144)):
+                todo.append((pb, None, None, None))
+        for pb, pst, pld, _ in todo:
+            distinct = pb.num_layers if pb.name == "l8b_pipe32" else 6
+            _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, {distinct} distinct layer data sets)")
+            pst = pst or measure_step(pb, 20, 3, min_warm_ms=200.0)
+            pld = pld or measure_load(pb, reps=4)
+            rec = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"], reps=2,
+                                   distinct=distinct)
+            rec["attn_tflops"] = attention_flops(pb.prefix_lens, pb.suffix_lens, pb.num_q_heads,
+                                                 pb.head_dim) / (pst["attn_ms"] * 1e-3) / 1e12
+            rec["load_GBps"] = pld[method]["GBps"]
+            pipelines[pb.name] = rec
+            if pb.name == "l8b_pipe32_s6144":
+                _say(f"[bench] offload: {pb.name}")
+                off, osrc, odst = measure_offload(pb)
+                extra["offload"] = off
+                for om, key in (("dma_staged", "dma_staged"), ("kernel_pull", "kernel_push")):
+                    _say(f"[bench] pipeline with offload ({key}): {pb.name}")
+                    pipelines[f"{pb.name}_offload_{key}"] = measure_pipeline_offload(
+                        pb, method, pld[method]["ms"], pst["step_ms"], off[key]["ms"], osrc, odst,
+                        offload_method=om, distinct=6)
     if not args.no_extra:
         _say("[bench] SSD tier: queue-window prefetch")
         extra["prefetch"] = measure_prefetch()
@@ -759,38 +961,23 @@ def _main(args, sampler):
         extra["decode"] = measure_decode()
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
-        rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=50.0)
+        rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=200.0)
         rfl = attention_flops(rb.prefix_lens, rb.suffix_lens, rb.num_q_heads, rb.head_dim)
-        extra["rag_mix"] = {"attn_ms": rst["attn_ms"], "step_ms": rst["step_ms"], "flops": rfl,
-                            "attn_tflops": rfl / (rst["attn_ms"] * 1e-3) / 1e12,
-                            "frac": rfl / (rst["attn_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
-                            "T": rb.T, "hit_ratio": rb.extra["hit_ratio"],
-                            "load_bytes": load_bytes(rb.prefix_lens, rb.num_kv_heads, rb.head_dim)}
-        if not args.no_pipeline:
-            ob = synth.l8b_pipe32(suffix=6144)
-            _say(f"[bench] offload: {ob.name}")
-            off, osrc, odst = measure_offload(ob)
-            extra["offload"] = off
-            for pb in (synth.l70b_pipe80(), synth.l8b_pipe32(suffix=6144)):
-                _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, 4 distinct layer data sets)")
-                pst = measure_step(pb, 10, 3, min_warm_ms=50.0)
-                pld = measure_load(pb, reps=4)
-                pipelines[pb.name] = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"],
-                                                      reps=2, distinct=4)
-                pipelines[pb.name]["attn_tflops"] = attention_flops(
-                    pb.prefix_lens, pb.suffix_lens, pb.num_q_heads, pb.head_dim) / (pst["attn_ms"] * 1e-3) / 1e12
-                pipelines[pb.name]["load_GBps"] = pld[method]["GBps"]
-                if pb.name == ob.name:
-                    _say(f"[bench] pipeline with offload: {pb.name}")
-                    for om, key in (("dma_staged", "dma_staged"), ("kernel_pull", "kernel_push")):
-                        pipelines[f"{pb.name}_offload_{key}"] = measure_pipeline_offload(
-                            pb, method, pld[method]["ms"], pst["step_ms"], off[key]["ms"], osrc, odst,
-                            offload_method=om)
-    cpu = None
+        extra["rag_mix"] = dict(_step_record(rb, rst), T=rb.T, hit_ratio=rb.extra["hit_ratio"],
+                                load_bytes=load_bytes(rb.prefix_lens, rb.num_kv_heads, rb.head_dim))
+        _say("[bench] append sweep")
+        extra["append_sweep"] = measure_append_sweep()
+        _say("[bench] prefix-tree hit ratio under capacity (host)")
+        extra["hit_ratio"] = hit_ratio_report()
+    cpu = legs = None
     if not args.no_cpu_baseline:
         _say("[bench] cpu baseline (oracle)")
         cpu = cpu_baseline(batch)
+        if not args.no_extra:
+            _say("[bench] cpu baseline legs (oracle)")
+            legs = cpu_baseline_legs(cpu)
 
+    headline_pipe = pipelines.get(batch.name)
     rec = {
         "metric": "prefix-reuse prefill TFLOP/s + % MFMA peak; exposed KV-load ms/layer",
         "value": value,
@@ -807,12 +994,16 @@ def _main(args, sampler):
         "config": {"workload": args.workload, "batch": batch.B, "num_q_heads": batch.num_q_heads,
                    "num_kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim,
                    "prefix_len": batch.prefix_lens[0], "suffix_len": batch.suffix_lens[0],
-                   "block_size": batch.block_size, "pool_blocks": batch.pool_blocks,
-                   "step": "append + attention, prefix KV resident in HBM"},
+                   "block_size": batch.block_size, "pool_blocks": batch.pool_blocks, "layers": batch.num_layers,
+                   "step": "one layer: append + attention, prefix KV resident in HBM",
+                   "warmup_calls": st["warmup_calls"]},
         "mfma_frac": value / MFMA_BF16_PEAK_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": "prefill_attn_kernel", "achieved": attn_tflops,
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
-                     "traffic": measured_traffic(), "flops_per_launch": flops, "avg_launch_ms": st["attn_ms"],
+                     "traffic": measured_traffic(batch.name), "flops_per_launch": flops,
+                     "avg_launch_ms": st["attn_ms"], "median_launch_ms": st["attn_ms_median"],
+                     "launch_ms_range": [st["attn_ms_min"], st["attn_ms_max"]],
+                     "timed": "HIP events around each attention launch inside the timed steps",
                      "sampled_clock_mhz": clocks["gfx_mhz_mean"] if clocks else None,
                      "peak_at_sampled_clock": (MFMA_BF16_PEAK_TFLOPS * clocks["gfx_mhz_mean"] / 2400.0
                                                if clocks else None),
@@ -822,17 +1013,16 @@ def _main(args, sampler):
         "append": {"ms": st["append_ms"], "bytes": app_b, "GBps": app_b / st["append_ms"] / 1e6,
                    "frac_hbm": app_b / st["append_ms"] / 1e6 / HBM_PEAK_GBS},
         "load": load,
-        "pipeline": pipe,
+        "pipeline": headline_pipe,
         "pipelines": pipelines or None,
-        "rag_mix": extra.get("rag_mix"),
-        "offload": extra.get("offload"),
-        "decode": extra.get("decode"),
-        "prefetch": extra.get("prefetch"),
-        "exposed_kv_load_ms_per_layer": pipe["exposed_ms_per_layer"] if pipe else None,
+        "exposed_kv_load_ms_per_layer": headline_pipe["exposed_ms_per_layer"] if headline_pipe else None,
         "cpu_baseline": cpu,
+        "cpu_baseline_legs": legs,
         "wall_s_timed": st["wall_s"],
         "wall_ms_per_step": st["wall_ms_per_step"],
     }
+    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "offload", "decode", "prefetch", "append_sweep",
+                                          "hit_ratio")})
     print(json.dumps(rec), flush=True)
     return 0
 

@@ -29,6 +29,8 @@ def open_library(path):
     lib.pcr_oracle_attention_rows.restype = ctypes.c_int
     lib.pcr_oracle_num_threads.argtypes = []
     lib.pcr_oracle_num_threads.restype = ctypes.c_int
+    lib.pcr_oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.pcr_oracle_set_num_threads.restype = None
     return lib
 
 
@@ -41,6 +43,12 @@ def _load():
 
 def num_threads() -> int:
     return int(_load().pcr_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the following oracle calls (timing runs only; results do not depend
+    on it: every output row is computed by one thread in a fixed order)."""
+    _load().pcr_oracle_set_num_threads(int(n))
 
 
 def _c(a, dtype):

@@ -160,13 +160,24 @@ int pcr_oracle_attention_rows(const uint16_t *q, int Hq, int Hkv, int d, int bs,
     return rc;
 }
 
-/* Number of threads the OpenMP runtime will use (for reporting). */
 #ifndef PCR_ORACLE_SOURCE_SHA256
 #define PCR_ORACLE_SOURCE_SHA256 "unknown"
 #endif
 /* SHA-256 of the source this library was built from (set by the build script). */
 const char *pcr_oracle_source_sha256(void) { return PCR_ORACLE_SOURCE_SHA256; }
 
+/* Threads for the next parallel regions (n >= 1), e.g. a one-thread timing run. */
+void pcr_oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}
+
+/* Number of threads the OpenMP runtime will use (for reporting). */
 int pcr_oracle_num_threads(void)
 {
     int n = 1;

@@ -33,8 +33,11 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     if not np.all(np.isfinite(x)):
         raise ValueError("f32_to_bf16_bits: non-finite input")
     u = x.view(np.uint32)
-    lsb = (u >> np.uint32(16)) & np.uint32(1)
-    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    r = u >> np.uint32(16)          # in place from here: (u + 0x7FFF + lsb) >> 16
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
     return r.astype(np.uint16)
 
 
@@ -195,6 +198,22 @@ def make_layer(batch: Batch, layer: int = 0, host_store: bool = True) -> LayerDa
     else:
         host_k = host_v = np.zeros((0, Hkv, bs * d), np.uint16)
     return LayerData(q=q, k_new=k_new, v_new=v_new, host_k=host_k, host_v=host_v)
+
+
+def make_layers(batch: Batch, layers: Sequence[int], host_store: bool = True, workers: int = 8) -> List[LayerData]:
+    """make_layer for several layers, drawn concurrently (each from its own layer seed, so
+    the result is the same as drawing them one by one)."""
+    from concurrent.futures import ThreadPoolExecutor
+    layers = list(layers)
+    with ThreadPoolExecutor(max(1, min(workers, len(layers)))) as ex:
+        return list(ex.map(lambda l: make_layer(batch, l, host_store), layers))
+
+
+def pipeline_data_sets(num_layers: int, distinct: int) -> List[int]:
+    """Which of `distinct` generated data sets each layer of a pipeline uses: layer l takes
+    set l % distinct. With distinct = num_layers every layer has its own data; with 6 sets
+    the first, middle and last layers of the 32- and 80-layer stacks all differ."""
+    return [l % max(1, min(distinct, num_layers)) for l in range(num_layers)]
 
 
 # ----------------------------------------------------------------------------
