@@ -514,11 +514,13 @@ def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
             "prefill_kernel_frac_hbm": nbytes / ms_prefill / 1e6 / HBM_PEAK_GBS}
 
 
-def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_chunks=96, request_compute_ms=30.0, n_serve=40):
+def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_sweep=(48, 96, 192), request_compute_ms=30.0,
+                     n_serve=40):
     """Serving loop through DRAM and SSD tiers with the queue-window prefetch: SSD stall
-    per request for each window size, on this machine's disk (O_DIRECT when the file
-    system allows it). Chunks are scaled to chunk_mib MiB; compute is a sleep of
-    request_compute_ms per 2500 computed tokens."""
+    per request for each window size and each DRAM capacity (in chunks), on this
+    machine's disk (O_DIRECT when the file system allows it), with the number of chunks
+    read ahead and then evicted before their request came. Chunks are scaled to
+    chunk_mib MiB; compute is a sleep of request_compute_ms per 2500 computed tokens."""
     import shutil
     import tempfile
     from paper_2603_23049_amd import prefetch, synth
@@ -526,17 +528,20 @@ def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_chunks=96, request_com
     base = os.path.join(ROOT, ".pytest_store")
     os.makedirs(base, exist_ok=True)
     d = tempfile.mkdtemp(dir=base)
-    out = {"chunk_bytes": chunk_mib << 20, "dram_chunks": dram_chunks, "requests": n_serve,
-           "compute_ms_per_2500_tokens": request_compute_ms}
+    out = {"chunk_bytes": chunk_mib << 20, "requests": n_serve, "compute_ms_per_2500_tokens": request_compute_ms,
+           "by_dram_chunks": {}}
     try:
-        for w in windows:
-            st = prefetch.serve(stream.requests, store_path=os.path.join(d, f"w{w}.bin"), chunk_bytes=chunk_mib << 20,
-                                dram_chunks=dram_chunks, window=w, compute_ms_per_token=request_compute_ms / 2500,
-                                io_threads=4)
-            out[f"window_{w}"] = {"stall_ms_per_request": st.stall_ms / max(st.requests, 1),
-                                  "on_demand_reads": st.on_demand_reads, "prefetch_reads": st.prefetch_reads,
-                                  "prefetch_hits": st.prefetch_hits, "dram_hits": st.dram_hits,
-                                  "wall_ms": st.wall_ms}
+        for dram_chunks in dram_sweep:
+            row = {}
+            for w in windows:
+                st = prefetch.serve(stream.requests, store_path=os.path.join(d, f"w{w}.bin"),
+                                    chunk_bytes=chunk_mib << 20, dram_chunks=dram_chunks, window=w,
+                                    compute_ms_per_token=request_compute_ms / 2500, io_threads=4)
+                row[f"window_{w}"] = {"stall_ms_per_request": st.stall_ms / max(st.requests, 1),
+                                      "on_demand_reads": st.on_demand_reads, "prefetch_reads": st.prefetch_reads,
+                                      "prefetch_hits": st.prefetch_hits, "dram_hits": st.dram_hits,
+                                      "prefetch_evicted_before_use": st.prefetch_evicted, "wall_ms": st.wall_ms}
+            out["by_dram_chunks"][str(dram_chunks)] = row
         probe = prefetch.page_aligned_buffer(chunk_mib << 20)
         from paper_2603_23049_amd import pcr
         store = pcr.ChunkStore(os.path.join(d, "probe.bin"), chunk_mib << 20, 4)

@@ -292,7 +292,25 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // first real score of the row, then rescale_thr = 8 / c, so P stays <= 2^8 and O is
     // rescaled rarely.
     float thr = -INFINITY;
-    float l_run[2] = {0.f, 0.f};   // this lane's part of the denominator (two chains)
+    // Row sums of the bf16 P on the matrix pipe (64 fewer VALU instructions per tile in
+    // the softmax than adding the rounded values there, for 4 short MFMAs that fill idle
+    // matrix-pipe cycles): v_mfma_f32_16x16x32_bf16 with B = a P^T
+    // operand of the second product (read in that instruction's layout: column c = lane%16
+    // takes the 8-key runs of lanes c, c+16, c+32, c+48, i.e. queries c and c+16, each over
+    // both key halves) and a constant A whose row m is 1 on the runs of query c when m is
+    // even and of query c+16 when m is odd. Per tile, four such products (one per P^T
+    // operand) start from zero; lane l then holds the tile's sum of query l%16 in
+    // tsum[0] and of query l%16+16 in tsum[1], i.e. of its own query (l%32) in
+    // tsum[(l >> 4) & 1]. The next softmax adds it to the running sum before any
+    // rescale, so the running sum stays one fp32 per lane.
+    f32x4 tsum = {0.f, 0.f, 0.f, 0.f};   // the last PV'd tile's sums (zero before the first)
+    float l_run = 0.f;                     // this lane's query: sum over the earlier tiles
+    bf16x8 sum_pat;
+    {
+        const __bf16 one = (((lane & 15) ^ (lane >> 4)) & 1) ? (__bf16)0.f : (__bf16)1.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum_pat[e] = one;
+    }
     f32x16 nbias;
 #pragma unroll
     for (int r = 0; r < 16; ++r) nbias[r] = 0.f;
@@ -385,6 +403,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
                 }
                 o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(raw), pf[t], o_acc[mt], 0, 0, 0);
             }
+            tsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sum_pat, pf[t], t == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : tsum,
+                                                           0, 0, 0);
         }
     };
 
@@ -442,6 +462,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             if (i < NPV) {
                 const int t = i / MT, mt = i % MT;
                 o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i]), pf[t], o_acc[mt], 0, 0, 0);
+                if (mt == MT - 1)
+                    tsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sum_pat, pf[t],
+                                                                   t == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : tsum, 0, 0, 0);
             } else {
                 const int m = (i - NPV) / KSTEPS, ks = (i - NPV) % KSTEPS;
                 st[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i]), qf[ks], ks == 0 ? nbias : st[m],
@@ -457,7 +480,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
         for (int i = 0; i < NALL; ++i) {
             if (i + kAhead < NALL) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < NPV && i % MT == MT - 1)   // PV MFMA, then the row-sum MFMA
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            else
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
@@ -465,6 +491,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 
     // ---- vector work: online softmax of S^T(j) into bf16 P(j) (lazy rescale) ----
     auto softmax = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+        l_run += (lane & 16) ? tsum[1] : tsum[0];   // tile j-1 (zero before the first tile)
         const int kbase = (tile_begin + j) * kTileKeys;
         if (kbase + kTileKeys - 1 > w_min_limit) {
             // register r of half tile m holds key kbase + 32m + 16(r/8) + 8half + r%8
@@ -506,8 +533,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             const float alpha = thr == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(-delta * scale_log2);
             thr = need ? rescale_thr : thr;
             m_ref += delta;
-            l_run[0] *= alpha;
-            l_run[1] *= alpha;
+            l_run *= alpha;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -519,13 +545,10 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) nbias[r] = -m_ref;
         }
-        // Row sums of the bf16-rounded probabilities, the same values the second product
-        // weights V with: the weights then sum to one however P rounds (a one-hot row
-        // returns its V row exactly), where a sum of the fp32 values would leave up to
-        // 2^-8 of relative error on a dominant term. Plain VALU adds: the bf16 dot
-        // instructions would need half the count, but they wait behind the other wave's
-        // MFMAs on this SIMD (measured about 70 cycles each), while the adds issue beside
-        // them.
+        // P rounded to bf16 is both the second product's operand and what the row sums
+        // add (on the matrix pipe, see tsum): the weights then sum to one however P
+        // rounds (a one-hot row returns its V row exactly), where a sum of the fp32
+        // values would leave up to 2^-8 of relative error on a dominant term.
 #pragma unroll
         for (int t = 0; t < kTileBlocks; ++t) {
             f32x8 pv8;
@@ -533,9 +556,6 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
             for (int e = 0; e < 8; ++e)
                 pv8[e] = __builtin_amdgcn_exp2f(st[t >> 1][8 * (t & 1) + e] * scale_log2);
             pf[t] = __builtin_convertvector(pv8, bf16x8);
-            const f32x8 pr = __builtin_convertvector(pf[t], f32x8);
-            l_run[0] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-            l_run[1] += (pr[4] + pr[5]) + (pr[6] + pr[7]);
         }
     };
 
@@ -635,8 +655,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // Each group finalises half of the head dims (group 0 the first MT/2 blocks of 32,
     // group 1 the rest): it sends the partner wave holding the same rows the other half
     // of its accumulator and its (m, l), then merges the half it received.
-    const float l_own = l_run[0] + l_run[1];
-    const float l_tot = l_own + __shfl_xor(l_own, 32);
+    const float l_tot = l_run + ((lane & 16) ? tsum[1] : tsum[0]);   // plus the group's last tile
     const bool has_ref = thr > -INFINITY;      // this row saw a real score in this key half
     constexpr int MH = MT / 2;
     constexpr int XW = 4 * MH + 1;                 // float4 slots per lane: half of O, then (m, l)

@@ -49,6 +49,7 @@ struct pcr_chunk_store {
     bool stop = false;
     std::vector<std::thread> workers;
     int64_t bytes_read = 0, bytes_written = 0;
+    int64_t direct_fallbacks = 0;   // transfers that O_DIRECT refused and the page cache served
 };
 
 namespace {
@@ -87,10 +88,20 @@ void worker(pcr_chunk_store *st)
         }
         const int64_t off = t.id * st->chunk_bytes;
         const int fd = (st->fd_direct >= 0 && page_aligned(t.buf, st->chunk_bytes)) ? st->fd_direct : st->fd;
-        const bool ok = xfer(fd, t.write, t.buf, st->chunk_bytes, off);
-        const int err = errno;
+        bool ok = xfer(fd, t.write, t.buf, st->chunk_bytes, off);
+        int err = errno;
+        bool fell_back = false;
+        if (!ok && fd == st->fd_direct && (err == EFAULT || err == EINVAL)) {
+            // Direct I/O pins the buffer's pages, which fails for host memory the GPU driver
+            // mapped (pinned memory from hipHostMalloc): such buffers go through the page
+            // cache instead (the kernel keeps the two kinds of access to the file coherent).
+            ok = xfer(st->fd, t.write, t.buf, st->chunk_bytes, off);
+            err = errno;
+            fell_back = true;
+        }
         {
             std::lock_guard<std::mutex> lk(st->mu);
+            st->direct_fallbacks += fell_back;
             if (!ok) {
                 if (!st->io_errors++)
                     snprintf(st->first_error, sizeof st->first_error, "%s of chunk %lld failed: %s",

@@ -42,6 +42,123 @@ def chunk_pattern(node_id: int, nbytes: int) -> np.ndarray:
     return np.random.Generator(np.random.PCG64(1_000_003 + node_id)).integers(0, 256, size=nbytes, dtype=np.uint8)
 
 
+class KVTier:
+    """The DRAM tier of KV chunks as pinned host memory on the data path, over the SSD
+    tier (Sec. 4.4: chunks are read from SSD into DRAM ahead of use and written back
+    after compute; Sec. 5: the load copies DRAM chunks to the GPU layer by layer).
+
+    For each of n_layers layers the DRAM tier is one pinned host store in the pool's
+    per-block layout (a pcr.HostKV, [n_slots * blocks_per_chunk][Hkv][bs*d] for K and
+    for V). Slot i of every layer holds one chunk: host blocks
+    [i * blocks_per_chunk, (i + 1) * blocks_per_chunk). So pcr_load_kv_layer copies a
+    resident chunk straight from its slot into the pool, and pcr_offload_kv_layer (or the
+    offload pipeline) writes a computed chunk straight into a slot. The SSD store keeps
+    one record per (chunk, layer, K or V) of blocks_per_chunk blocks, id
+    (node_id * n_layers + layer) * 2 + part. Slots are page-aligned, so the store's reads
+    and writes bypass the page cache. Slots are evicted least recently used first, never
+    one that is protected, being read, or whose write-back is still in flight (the
+    eviction waits for it)."""
+
+    def __init__(self, store_path: str, n_slots: int, n_layers: int, num_kv_heads: int, head_dim: int,
+                 block_size: int = 16, chunk_tokens: int = 256, io_threads: int = 4):
+        import torch
+        self.bpc = chunk_tokens // block_size
+        self.n_slots, self.n_layers = n_slots, n_layers
+        shape = (n_slots * self.bpc, num_kv_heads, block_size * head_dim)
+        self.layers = [pcr.HostKV(torch.zeros(shape, dtype=torch.int16, pin_memory=True),
+                                  torch.zeros(shape, dtype=torch.int16, pin_memory=True), num_kv_heads, head_dim,
+                                  block_size) for _ in range(n_layers)]
+        self.part_bytes = self.bpc * num_kv_heads * block_size * head_dim * 2
+        for h in self.layers:
+            for t in (h.k, h.v):
+                if t.data_ptr() % mmap.PAGESIZE:
+                    raise RuntimeError("pinned DRAM tier is not page-aligned")
+        self.store = pcr.ChunkStore(store_path, self.part_bytes, io_threads)
+        self.free = list(range(n_slots))[::-1]
+        self.where: "OrderedDict[int, int]" = OrderedDict()   # node id -> slot, least recent first
+        self.reading: Dict[int, int] = {}
+        self.on_ssd: set = set()
+        self.evictions = 0
+
+    def _rid(self, nid: int, layer: int, part: int) -> int:
+        return (nid * self.n_layers + layer) * 2 + part
+
+    def part(self, layer: int, slot: int, part: int):
+        """The pinned view of one slot's K (part 0) or V (part 1) blocks of a layer."""
+        h = self.layers[layer]
+        return (h.k if part == 0 else h.v)[slot * self.bpc:(slot + 1) * self.bpc]
+
+    def slot_blocks(self, slot: int) -> np.ndarray:
+        return np.arange(slot * self.bpc, (slot + 1) * self.bpc, dtype=np.int32)
+
+    def slot_of(self, nid: int) -> int:
+        return self.where[nid]
+
+    def resident(self, nid: int) -> bool:
+        return nid in self.where
+
+    def touch(self, nid: int):
+        if nid in self.where:
+            self.where.move_to_end(nid)
+
+    def alloc(self, nid: int, protect: set) -> Optional[int]:
+        """A slot for chunk nid (evicting the least recently used unprotected chunk), or None."""
+        if self.free:
+            slot = self.free.pop()
+        else:
+            slot = None
+            for old in self.where:
+                if old in protect or old in self.reading:
+                    continue
+                slot = self.where.pop(old)
+                for l in range(self.n_layers):          # its write-back must finish before reuse
+                    self.store.wait(self._rid(old, l, 0))
+                    self.store.wait(self._rid(old, l, 1))
+                self.evictions += 1
+                break
+            if slot is None:
+                return None
+        self.where[nid] = slot
+        return slot
+
+    def start_read(self, nid: int, protect: set) -> bool:
+        """Issue the SSD reads of every layer of chunk nid into a DRAM slot."""
+        slot = self.alloc(nid, protect)
+        if slot is None:
+            return False
+        for l in range(self.n_layers):
+            for part in (0, 1):
+                self.store.read_async(self._rid(nid, l, part), self.part(l, slot, part))
+        self.reading[nid] = slot
+        return True
+
+    def finish_read(self, nid: int):
+        if nid in self.reading:
+            for l in range(self.n_layers):
+                self.store.wait(self._rid(nid, l, 0))
+                self.store.wait(self._rid(nid, l, 1))
+            del self.reading[nid]
+
+    def write_back(self, nid: int):
+        """Queue the SSD writes of every layer of a resident chunk (asynchronous)."""
+        slot = self.where[nid]
+        for l in range(self.n_layers):
+            for part in (0, 1):
+                self.store.write_async(self._rid(nid, l, part), self.part(l, slot, part))
+        self.on_ssd.add(nid)
+
+    def drop(self, nid: int):
+        """Forget the DRAM copy of a chunk (after its write-back has finished)."""
+        slot = self.where.pop(nid)
+        for l in range(self.n_layers):
+            self.store.wait(self._rid(nid, l, 0))
+            self.store.wait(self._rid(nid, l, 1))
+        self.free.append(slot)
+
+    def close(self):
+        self.store.close()
+
+
 @dataclass
 class ServeStats:
     requests: int = 0
@@ -53,6 +170,7 @@ class ServeStats:
     prefetch_hits: int = 0          # needed chunks whose read was already issued by the prefetcher
     dram_hits: int = 0              # needed chunks already resident in DRAM
     writes: int = 0
+    prefetch_evicted: int = 0       # chunks read ahead but evicted from DRAM before their request
     wall_ms: float = 0.0
 
 
@@ -67,6 +185,8 @@ class TieredCache:
         self.where: "OrderedDict[int, int]" = OrderedDict()   # node id -> slot, least recent first
         self.reading: Dict[int, int] = {}                       # node id -> slot with a read in flight
         self.on_ssd: set = set()
+        self.prefetched: set = set()       # read ahead and not used yet
+        self.prefetch_evicted = 0          # chunks read ahead and evicted before their request came
 
     def _slot(self, protect: set) -> Optional[int]:
         if self.free:
@@ -76,6 +196,9 @@ class TieredCache:
                 continue
             slot = self.where.pop(nid)
             self.store.wait(nid)           # a write-back of this slot must finish before reuse
+            if nid in self.prefetched:
+                self.prefetched.discard(nid)
+                self.prefetch_evicted += 1
             return slot
         return None
 
@@ -151,6 +274,7 @@ def serve(requests: Sequence[Sequence[int]], *, store_path: str, chunk_bytes: in
                     if nid in cache.on_ssd and not cache.resident(nid):
                         if cache.start_read(nid, protect=protect):
                             st.prefetch_reads += 1
+                            cache.prefetched.add(nid)
             t0 = time.perf_counter()
             for nid in need:
                 if nid in cache.reading:
@@ -163,6 +287,7 @@ def serve(requests: Sequence[Sequence[int]], *, store_path: str, chunk_bytes: in
                     st.on_demand_reads += 1
                 cache.finish_read(nid)
                 cache.touch(nid)
+                cache.prefetched.discard(nid)
             st.stall_ms += (time.perf_counter() - t0) * 1e3
             if verify:
                 for nid in need:
@@ -180,6 +305,7 @@ def serve(requests: Sequence[Sequence[int]], *, store_path: str, chunk_bytes: in
             st.requests += 1
         store.wait()
         st.wall_ms = (time.perf_counter() - t_start) * 1e3
+        st.prefetch_evicted = cache.prefetch_evicted
     finally:
         store.close()
     return st

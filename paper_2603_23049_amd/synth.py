@@ -209,6 +209,16 @@ def make_layers(batch: Batch, layers: Sequence[int], host_store: bool = True, wo
         return list(ex.map(lambda l: make_layer(batch, l, host_store), layers))
 
 
+def chunk_kv(node_id: int, layer: int, num_kv_heads: int, head_dim: int, blocks_per_chunk: int = 16,
+             bs: int = BLOCK_SIZE):
+    """K and V payload of one cached chunk of one layer, [blocks_per_chunk][Hkv][bs*d] bf16
+    bits each, drawn from a seed derived from the tree node id and the layer (stands for
+    the KV a model would have computed for that chunk)."""
+    rng = np.random.Generator(np.random.PCG64(7_000_003 * (node_id + 1) + layer))
+    shape = (blocks_per_chunk, num_kv_heads, bs * head_dim)
+    return normal_bf16(rng, shape), normal_bf16(rng, shape)
+
+
 def pipeline_data_sets(num_layers: int, distinct: int) -> List[int]:
     """Which of `distinct` generated data sets each layer of a pipeline uses: layer l takes
     set l % distinct. With distinct = num_layers every layer has its own data; with 6 sets
