@@ -278,6 +278,29 @@ pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t
                            int64_t workspace_bytes, void *stream);
 
 /*
+ * pcr_decode_attn_noalloc -- pcr_decode_attn without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc). Same arguments, result and
+ * numerics as pcr_decode_attn; the partial results of the chunk merge go to a
+ * scratch array of PCR_DECODE_NOALLOC_SCRATCH_BYTES (16 MiB) that the library
+ * holds per device until the process ends (its address is taken on the first call
+ * on each device). The call allocates nothing and calls no allocating routine.
+ * Every call on one device shares that device's scratch, which keeps the last
+ * call's contents (nothing needs clearing: each call writes every entry it reads
+ * back), so calls on one device that may overlap (different streams, or host
+ * threads without ordering) race; order them on one stream.
+ * Errors: as pcr_decode_attn, and PCR_ERR_UNSUPPORTED when the batch would need
+ * more scratch than the maximum (pcr_decode_attn_workspace_size tells the size;
+ * at most about 11 MiB for any batch on a 256-compute-unit GPU); the message
+ * names both sizes.
+ */
+#define PCR_DECODE_NOALLOC_SCRATCH_BYTES (16 << 20)
+pcr_status pcr_decode_attn_noalloc(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                                   int32_t max_blocks, const int32_t *context_lens,
+                                   const int32_t *host_context_lens, int32_t B, int32_t num_q_heads,
+                                   float sm_scale, void *out, void *stream);
+
+/*
  * pcr_decode_attn_workspace_size -- bytes of workspace pcr_decode_attn needs on the
  * current device for any batch of B sequences whose context lengths are at most
  * max_context (0 when every such batch is handled without one). Queries the

@@ -35,8 +35,16 @@
 // writes its unnormalised O, max and sum to the workspace and
 // decode_combine_kernel merges the chunks of each (sequence, head).
 #include <algorithm>
+#include <mutex>
 
 #include "pcr_internal.h"
+
+// Scratch of the allocation-free decode entry point: the split kernel's partial
+// outputs (O, max, sum per chunk and query head) when a batch's chunks merge
+// through memory. One copy per device, held until the process ends. In host code
+// this name is a stand-in, not a device address: kernels get the address that
+// hipGetSymbolAddress returns for the current device (decode_noalloc_scratch).
+static __device__ __align__(256) unsigned char scratch[pcr::kDecodeScratchBytes];
 
 namespace pcr {
 namespace {
@@ -322,6 +330,30 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(
 }
 
 }  // namespace
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, once taken
+}  // namespace
+
+hipError_t decode_noalloc_scratch(void **ptr)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // this device's copy (the device is current)
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                        int32_t max_context, int32_t n_cu)

@@ -66,6 +66,11 @@ int decode_max_cols();
 hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int32_t *block_tables,
                               int32_t max_blocks, const int32_t *context_lens, int32_t B, int32_t num_q_heads,
                               const DecodePlan &plan, float sm_scale, void *out, void *workspace, hipStream_t s);
+// Size of the allocation-free decode entry point's per-device scratch (decode.hip),
+// and its device address on the current device (taken with hipGetSymbolAddress on the
+// first call per device, then reused).
+constexpr int64_t kDecodeScratchBytes = PCR_DECODE_NOALLOC_SCRATCH_BYTES;
+hipError_t decode_noalloc_scratch(void **ptr);
 
 // Pool-to-host offload with any method (the staged one takes the workspace); used by
 // the pipeline, which chooses the method per call.

@@ -697,13 +697,16 @@ pcr_status pcr_decode_attn_workspace_size(int32_t B, int32_t num_q_heads, int32_
     return PCR_OK;
 }
 
-pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
-                           const int32_t *context_lens, const int32_t *host_context_lens, int32_t B,
-                           int32_t num_q_heads, float sm_scale, void *out, void *workspace, int64_t workspace_bytes,
-                           void *stream)
+}  // extern "C"
+
+// Every host-side check of the decode entry points; on success *plan is the launch plan
+// (plan->n_split == 0: nothing to do).
+static pcr_status decode_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                               int32_t max_blocks, const int32_t *context_lens, const int32_t *host_context_lens,
+                               int32_t B, int32_t num_q_heads, float sm_scale, const void *out, const char *who,
+                               DecodePlan *plan)
 {
-    g_err[0] = 0;
-    const char *who = "pcr_decode_attn";
+    *plan = DecodePlan{};
     pcr_status st = check_pool(pool, who);
     if (st) return st;
     if (B < 0) return fail(PCR_ERR_INVALID_ARG, "%s: B < 0", who);
@@ -731,7 +734,49 @@ pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t
     int32_t n_cu = 0;
     st = device_cu_count(&n_cu, who);
     if (st) return st;
-    const DecodePlan plan = decode_plan(B, num_q_heads, pool->num_kv_heads, pool->head_dim, max_ctx, n_cu);
+    *plan = decode_plan(B, num_q_heads, pool->num_kv_heads, pool->head_dim, max_ctx, n_cu);
+    return PCR_OK;
+}
+
+extern "C" {
+
+pcr_status pcr_decode_attn_noalloc(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                                   int32_t max_blocks, const int32_t *context_lens,
+                                   const int32_t *host_context_lens, int32_t B, int32_t num_q_heads,
+                                   float sm_scale, void *out, void *stream)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_decode_attn_noalloc";
+    DecodePlan plan;
+    pcr_status st = decode_check(q, pool, block_tables, max_blocks, context_lens, host_context_lens, B, num_q_heads,
+                                 sm_scale, out, who, &plan);
+    if (st || plan.n_split == 0) return st;
+    void *ws = nullptr;
+    if (plan.workspace_bytes > 0) {
+        if (plan.workspace_bytes > kDecodeScratchBytes)
+            return fail(PCR_ERR_UNSUPPORTED, "%s: this batch needs %lld bytes of scratch; the allocation-free entry "
+                        "point holds %lld (use pcr_decode_attn with a workspace)", who,
+                        (long long)plan.workspace_bytes, (long long)kDecodeScratchBytes);
+        hipError_t e = decode_noalloc_scratch(&ws);
+        if (e != hipSuccess) return hip_fail(e, "pcr_decode_attn_noalloc: scratch address");
+    }
+    hipError_t e = launch_decode_attn(q, *pool, block_tables, max_blocks, context_lens, B, num_q_heads, plan,
+                                      sm_scale, out, ws, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "pcr_decode_attn_noalloc: launch");
+    return PCR_OK;
+}
+
+pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
+                           const int32_t *context_lens, const int32_t *host_context_lens, int32_t B,
+                           int32_t num_q_heads, float sm_scale, void *out, void *workspace, int64_t workspace_bytes,
+                           void *stream)
+{
+    g_err[0] = 0;
+    const char *who = "pcr_decode_attn";
+    DecodePlan plan;
+    pcr_status st = decode_check(q, pool, block_tables, max_blocks, context_lens, host_context_lens, B, num_q_heads,
+                                 sm_scale, out, who, &plan);
+    if (st || plan.n_split == 0) return st;
     if (plan.workspace_bytes > 0) {
         if (!workspace || workspace_bytes < plan.workspace_bytes)
             return fail(PCR_ERR_INVALID_ARG, "%s: this batch needs a workspace of %lld bytes (%lld given)", who,

@@ -22,6 +22,8 @@ PCR_ERR_UNSUPPORTED = -2
 PCR_ERR_NOT_PINNED = -3
 PCR_ERR_HIP = -4
 
+DECODE_NOALLOC_SCRATCH_BYTES = 16 << 20   # PCR_DECODE_NOALLOC_SCRATCH_BYTES
+
 LOAD_AUTO = 0
 LOAD_DMA_BATCH = 1
 LOAD_DMA_PER_BLOCK = 2
@@ -33,7 +35,7 @@ LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block":
 EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_layer_method",
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
-           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
+           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
            "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
            "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
 
@@ -89,6 +91,8 @@ def lib():
                                               ctypes.c_float, P, P]
         L.pcr_decode_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, ctypes.c_float, P, P,
                                       i64, P]
+        L.pcr_decode_attn_noalloc.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, ctypes.c_float, P,
+                                              P]
         L.pcr_decode_attn_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int64)]
         L.pcr_gather_kv.argtypes = [ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, P, P, P]
         L.pcr_pipeline_run.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), ctypes.c_int, P, P,
@@ -332,6 +336,20 @@ def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, 
     _check(lib().pcr_decode_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
                                  _ptr(context_lens), _ptr(hcl), B, int(num_q_heads), float(sm_scale), _ptr(out),
                                  _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def decode_attn_noalloc(q, pool: KVPool, block_tables, context_lens, host_context_lens, num_q_heads: int, out,
+                        sm_scale: Optional[float] = None, stream=None):
+    """pcr_decode_attn_noalloc: as decode_attn, with the library's per-device scratch in
+    place of a workspace (nothing is allocated)."""
+    hcl = _i32_host(host_context_lens)
+    B = int(hcl.shape[0])
+    if sm_scale is None:
+        sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    p = pool.c()
+    _check(lib().pcr_decode_attn_noalloc(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
+                                         _ptr(context_lens), _ptr(hcl), B, int(num_q_heads), float(sm_scale),
+                                         _ptr(out), _stream(stream)))
 
 
 def gather_kv(pool: KVPool, block_tables, starts, cu_out, total: int, k_out, v_out, stream=None):
