@@ -555,7 +555,9 @@ def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_sweep=(48, 96, 192), r
         store.wait()
         dt = time.perf_counter() - t0
         out["ssd_read_GBps"] = 16 * (chunk_mib << 20) / dt / 1e9
-        out["direct_io"] = store.stats()["direct_io"]
+        sts = store.stats()
+        out["direct_io"] = sts["direct_io"]
+        out["direct_fallbacks"] = sts["direct_fallbacks"]
         store.close()
         del probe
     finally:

@@ -428,7 +428,11 @@ pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_k
  *   pcr_store_wait          block until chunk_id's tasks (or, for chunk_id < 0, all
  *                           tasks) are done; reports the first I/O error, if any
  *   pcr_store_poll          *done = 1 if nothing is pending for chunk_id (or at all)
- *   pcr_store_stats         bytes moved so far, and whether O_DIRECT is in use
+ *   pcr_store_stats         bytes moved so far; whether the file is open for O_DIRECT;
+ *                           and how many page-aligned transfers O_DIRECT refused (host
+ *                           memory the GPU driver mapped, such as hipHostMalloc pinned
+ *                           memory) and the page cache served instead
+ * Any output pointer of pcr_store_stats may be NULL.
  *   pcr_store_close         drain the queue, stop the threads, close the file
  */
 typedef struct pcr_chunk_store pcr_chunk_store;
@@ -437,7 +441,8 @@ pcr_status pcr_store_write_async(pcr_chunk_store *store, int64_t chunk_id, const
 pcr_status pcr_store_read_async(pcr_chunk_store *store, int64_t chunk_id, void *dst);
 pcr_status pcr_store_wait(pcr_chunk_store *store, int64_t chunk_id);
 pcr_status pcr_store_poll(pcr_chunk_store *store, int64_t chunk_id, int32_t *done);
-pcr_status pcr_store_stats(pcr_chunk_store *store, int64_t *bytes_read, int64_t *bytes_written, int32_t *direct);
+pcr_status pcr_store_stats(pcr_chunk_store *store, int64_t *bytes_read, int64_t *bytes_written, int32_t *direct,
+                           int64_t *direct_fallbacks);
 pcr_status pcr_store_close(pcr_chunk_store *store);
 
 /* Message of the last failed call on this thread ("" if none). */

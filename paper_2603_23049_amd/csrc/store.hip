@@ -193,13 +193,15 @@ pcr_status pcr_store_poll(pcr_chunk_store *st, int64_t chunk_id, int32_t *done)
     return PCR_OK;
 }
 
-pcr_status pcr_store_stats(pcr_chunk_store *st, int64_t *bytes_read, int64_t *bytes_written, int32_t *direct)
+pcr_status pcr_store_stats(pcr_chunk_store *st, int64_t *bytes_read, int64_t *bytes_written, int32_t *direct,
+                           int64_t *direct_fallbacks)
 {
     if (!st) return pcr::fail(PCR_ERR_INVALID_ARG, "pcr_store_stats: NULL store");
     std::lock_guard<std::mutex> lk(st->mu);
     if (bytes_read) *bytes_read = st->bytes_read;
     if (bytes_written) *bytes_written = st->bytes_written;
     if (direct) *direct = st->fd_direct >= 0;
+    if (direct_fallbacks) *direct_fallbacks = st->direct_fallbacks;
     return PCR_OK;
 }
 

@@ -112,7 +112,7 @@ def lib():
         L.pcr_store_read_async.argtypes = [P, i64, P]
         L.pcr_store_wait.argtypes = [P, i64]
         L.pcr_store_poll.argtypes = [P, i64, P]
-        L.pcr_store_stats.argtypes = [P, P, P, P]
+        L.pcr_store_stats.argtypes = [P, P, P, P, P]
         L.pcr_store_close.argtypes = [P]
         for name in EXPORTS:
             if name not in ("pcr_last_error", "pcr_version"):
@@ -484,9 +484,11 @@ class ChunkStore:
         return bool(d.value)
 
     def stats(self):
-        r, w, d = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int32(0)
-        _check(lib().pcr_store_stats(self._h, ctypes.addressof(r), ctypes.addressof(w), ctypes.addressof(d)))
-        return {"bytes_read": r.value, "bytes_written": w.value, "direct_io": bool(d.value)}
+        r, w, d, fb = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int32(0), ctypes.c_int64(0)
+        _check(lib().pcr_store_stats(self._h, ctypes.addressof(r), ctypes.addressof(w), ctypes.addressof(d),
+                                     ctypes.addressof(fb)))
+        return {"bytes_read": r.value, "bytes_written": w.value, "direct_io": bool(d.value),
+                "direct_fallbacks": fb.value}
 
     def close(self):
         if self._h:

@@ -143,6 +143,7 @@ def test_ssd_dram_pool_offload_round_trip(scratch):
         assert moved > 0
         st = tier.store.stats()
         say(f"    {len(new_nodes)} computed chunks offloaded, written back and read back; "
-            f"SSD read {st['bytes_read'] >> 20} MiB, written {st['bytes_written'] >> 20} MiB, O_DIRECT={st['direct_io']}")
+            f"SSD read {st['bytes_read'] >> 20} MiB, written {st['bytes_written'] >> 20} MiB, O_DIRECT={st['direct_io']}, "
+            f"{st['direct_fallbacks']} transfers through the page cache")
     finally:
         tier.close()
