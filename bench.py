@@ -369,9 +369,18 @@ def measure_step(batch, steps, warmup, min_warm_ms=500.0):
     e2.record(s)
     e2.synchronize()
     append_ms = a2.elapsed_time(e2) / steps
+    # the attention alone, back to back under one event pair (no per-launch gaps: for a
+    # short launch the per-launch events above add several microseconds each)
+    a3, e3 = ev(), ev()
+    a3.record(s)
+    for _ in range(steps):
+        _attn(L, bp, s)
+    e3.record(s)
+    e3.synchronize()
     return dict(step_ms=float(step_ms), wall_ms_per_step=wall / steps * 1e3, append_ms=append_ms,
                 attn_ms=attn_ms, attn_ms_min=float(min(launches)), attn_ms_max=float(max(launches)),
-                attn_ms_median=_median(launches), wall_s=wall, warmup_calls=warmup + warm_calls)
+                attn_ms_median=_median(launches), attn_b2b_ms=a3.elapsed_time(e3) / steps, wall_s=wall,
+                warmup_calls=warmup + warm_calls)
 
 
 def measure_load(batch, reps=10):
@@ -815,7 +824,21 @@ def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8,
                     "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS})
         del pool, k, v, slots, perm
     torch.cuda.synchronize()
-    return {"sizes": out, "asymptotic_GBps": out[-1]["GBps"], "asymptotic_frac_hbm": out[-1]["frac_hbm"]}
+    # reference: a plain device copy of 256 MiB (read + write, like the append)
+    src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    fn = lambda: dst.copy_(src)
+    warm_up(fn, 30.0)
+    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        fn()
+    e.record(s)
+    e.synchronize()
+    copy_gbps = 2 * (256 << 20) / (a.elapsed_time(e) / reps) / 1e6
+    del src, dst
+    return {"sizes": out, "asymptotic_GBps": out[-1]["GBps"], "asymptotic_frac_hbm": out[-1]["frac_hbm"],
+            "device_copy_256MiB_GBps": copy_gbps, "asymptotic_frac_of_device_copy": out[-1]["GBps"] / copy_gbps}
 
 
 def main(argv=None):
@@ -877,12 +900,12 @@ def main(argv=None):
 
 def _step_record(batch, st):
     flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
-    return {"workload": batch.name, "ms_per_step": st["step_ms"], "attn_ms": st["attn_ms"],
-            "attn_ms_median": st["attn_ms_median"], "append_ms": st["append_ms"], "flops": flops,
+    return {"workload": batch.name, "ms_per_step": st["step_ms"], "attn_ms": st["attn_b2b_ms"],
+            "attn_ms_in_step_events": st["attn_ms"], "append_ms": st["append_ms"], "flops": flops,
             "step_tflops": flops / (st["step_ms"] * 1e-3) / 1e12,
-            "attn_tflops": flops / (st["attn_ms"] * 1e-3) / 1e12,
-            "attn_frac": flops / (st["attn_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
-            "warmup_calls": st["warmup_calls"]}
+            "attn_tflops": flops / (st["attn_b2b_ms"] * 1e-3) / 1e12,
+            "attn_frac": flops / (st["attn_b2b_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "attn_timing": "back to back, one event pair over the launches", "warmup_calls": st["warmup_calls"]}
 
 
 def _main(args, sampler):
@@ -949,7 +972,7 @@ def _main(args, sampler):
             rec = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"], reps=2,
                                    distinct=distinct)
             rec["attn_tflops"] = attention_flops(pb.prefix_lens, pb.suffix_lens, pb.num_q_heads,
-                                                 pb.head_dim) / (pst["attn_ms"] * 1e-3) / 1e12
+                                                 pb.head_dim) / (pst["attn_b2b_ms"] * 1e-3) / 1e12
             rec["load_GBps"] = pld[method]["GBps"]
             pipelines[pb.name] = rec
             if pb.name == "l8b_pipe32_s6144":
@@ -972,6 +995,13 @@ def _main(args, sampler):
         rfl = attention_flops(rb.prefix_lens, rb.suffix_lens, rb.num_q_heads, rb.head_dim)
         extra["rag_mix"] = dict(_step_record(rb, rst), T=rb.T, hit_ratio=rb.extra["hit_ratio"],
                                 load_bytes=load_bytes(rb.prefix_lens, rb.num_kv_heads, rb.head_dim))
+        tb = synth.uniform_batch("l70b_tp8_shard", B=2, Hq=8, Hkv=1, d=128, p=15360, s=1024, pool_blocks=4096,
+                                 seed=5)
+        _say("[bench] one GPU's share of the 70B-shaped layer at tensor parallelism 8 (Hq 8, Hkv 1)")
+        tst = measure_step(tb, max(20, args.steps // 2), 3, min_warm_ms=200.0)
+        tld = measure_load(tb, reps=6)
+        extra["tp8_shard"] = dict(_step_record(tb, tst), load_ms=tld["kernel_pull"]["ms"],
+                                  load_GBps=tld["kernel_pull"]["GBps"], load_bytes=tld["bytes_per_layer"])
         _say("[bench] append sweep")
         extra["append_sweep"] = measure_append_sweep()
         _say("[bench] prefix-tree hit ratio under capacity (host)")
@@ -1010,6 +1040,7 @@ def _main(args, sampler):
                      "traffic": measured_traffic(batch.name), "flops_per_launch": flops,
                      "avg_launch_ms": st["attn_ms"], "median_launch_ms": st["attn_ms_median"],
                      "launch_ms_range": [st["attn_ms_min"], st["attn_ms_max"]],
+                     "back_to_back_launch_ms": st["attn_b2b_ms"],
                      "timed": "HIP events around each attention launch inside the timed steps",
                      "sampled_clock_mhz": clocks["gfx_mhz_mean"] if clocks else None,
                      "peak_at_sampled_clock": (MFMA_BF16_PEAK_TFLOPS * clocks["gfx_mhz_mean"] / 2400.0
@@ -1028,8 +1059,8 @@ def _main(args, sampler):
         "wall_s_timed": st["wall_s"],
         "wall_ms_per_step": st["wall_ms_per_step"],
     }
-    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "offload", "decode", "prefetch", "append_sweep",
-                                          "hit_ratio")})
+    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "prefetch",
+                                          "append_sweep", "hit_ratio")})
     print(json.dumps(rec), flush=True)
     return 0
 
