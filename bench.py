@@ -407,6 +407,38 @@ def measure_load(batch, reps=10):
             out[method] = {"ms": ms, "GBps": nbytes / ms / 1e6}
         except Exception as ex:  # a method this runtime lacks
             out[method] = {"error": str(ex)[:200]}
+    # staged: copy-engine transfers into a workspace, then the scatter kernel; the
+    # transfers alone (the same bytes host to workspace) give the two stages' times
+    ws = torch.empty(pcr.staged_workspace_bytes(len(bp.src_blocks), batch.num_kv_heads, batch.head_dim),
+                     dtype=torch.uint8, device="cuda")
+    half = nbytes // 2
+    hk = L.host.k.view(-1).view(torch.uint8)[:half]
+    hv = L.host.v.view(-1).view(torch.uint8)[:half]
+
+    def transfers():
+        with torch.cuda.stream(s):
+            ws[:half].copy_(hk, non_blocking=True)
+            ws[half:].copy_(hv, non_blocking=True)
+
+    def staged():
+        pcr.load_kv_layer(L.host, bp.src_blocks, L.pool, bp.dst_blocks, method="dma_staged", stream=s, workspace=ws)
+
+    stg = {}
+    for key, fn in (("ms", staged), ("transfer_ms", transfers)):
+        times = []
+        for r in range(reps + 2):
+            a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            fn()
+            e.record(s)
+            e.synchronize()
+            if r >= 2:
+                times.append(a.elapsed_time(e))
+        stg[key] = _median(times)
+    stg["GBps"] = nbytes / stg["ms"] / 1e6
+    stg["scatter_ms"] = max(stg["ms"] - stg["transfer_ms"], 0.0)
+    out["dma_staged"] = stg
+    del ws
     big = 256 << 20
     h = torch.empty(big, dtype=torch.uint8, pin_memory=True)
     h.fill_(1)
@@ -444,23 +476,36 @@ def _bracketed_ms(run, start_stream, end_stream, reps):
     return min(times)
 
 
-def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinct=None):
-    """The n-layer two-stream pipeline. Exposure per layer is the pipeline's time per
-    layer beyond the layer's isolated compute; its least possible value follows from
-    the isolated per-layer load and compute times (two in-order queues). The total
-    comes from untimed runs; one timed run gives the per-layer breakdown. With
-    `distinct`, only that many layers' host/Q/K/V data are generated and reused
-    round-robin (every layer still has its own pool and moves its own bytes)."""
+def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinct=None, staged_stages=None,
+                     layers_bp=None):
+    """The n-layer pipeline. Exposure per layer is the pipeline's time per layer beyond
+    the layer's isolated compute; its least possible value follows from the isolated
+    per-layer load and compute times (two in-order queues; for method "staged", the
+    three stages transfer, scatter and compute from `staged_stages` = (transfer ms,
+    scatter ms)). The total comes from untimed runs; one timed run gives the per-layer
+    breakdown. With `distinct`, only that many layers' host/Q/K/V data are generated and
+    reused round-robin (every layer still has its own pool and moves its own bytes).
+    Method "staged" runs pcr_pipeline_run_staged with two workspace slots."""
     import torch
     from paper_2603_23049_amd import pcr
     n = batch.num_layers
-    layers, bp = _setup_pipeline(batch, distinct or n)
+    layers, bp = layers_bp or _setup_pipeline(batch, distinct or n)
     copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
-    total = _bracketed_ms(lambda: pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method), comp_s, comp_s,
-                          reps)
-    best = pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method, timing=True)
+    if method == "staged":
+        scat_s = torch.cuda.Stream()
+        ws = torch.empty(2 * pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), batch.num_kv_heads, batch.head_dim),
+                         dtype=torch.uint8, device="cuda")
+        run = lambda timing=False: pcr.pipeline_run_staged(layers, bp, ws, copy_s, scat_s, comp_s, timing=timing)
+    else:
+        run = lambda timing=False: pcr.pipeline_run(layers, bp, copy_s, comp_s, method=method, timing=timing)
+    total = _bracketed_ms(lambda: run(), comp_s, comp_s, reps)
+    best = run(timing=True)
     e_raw = total / n - compute_ms_iso
-    e_min = flow_shop_exposure(load_ms_iso, compute_ms_iso, n) / n
+    if method == "staged":
+        bound = flow_shop3_makespan(staged_stages[0], staged_stages[1], compute_ms_iso, n)
+    else:
+        bound = flow_shop_exposure(load_ms_iso, compute_ms_iso, n) + n * compute_ms_iso
+    e_min = bound / n - compute_ms_iso
     del layers
     torch.cuda.synchronize()
     return {"layers": n, "workload": batch.name, "method": method, "distinct_layer_data": distinct or n,
@@ -473,7 +518,7 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
             "exposed_over_min_ms_per_layer": e_raw - e_min,
             "exposed_over_min_frac_of_load": (e_raw - e_min) / load_ms_iso if load_ms_iso > 0 else None,
             "exposed_frac_of_load": e_raw / load_ms_iso if load_ms_iso > 0 else None,
-            "bound_makespan_ms": flow_shop_exposure(load_ms_iso, compute_ms_iso, n) + n * compute_ms_iso,
+            "bound_makespan_ms": bound,
             "exposed_ideal_ms_per_layer": load_ms_iso / n if compute_ms_iso >= load_ms_iso else None}
 
 
@@ -858,7 +903,11 @@ def main(argv=None):
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the secondary lines (8B layer, RAG mix, decode, SSD tier, offload, append sweep, "
                          "hit ratios) and the 80-layer and compute-bound pipelines")
-    ap.add_argument("--pipeline-method", default="auto")
+    ap.add_argument("--pipeline-method", default="auto", choices=("auto", "kernel_pull", "staged", "dma_per_block"),
+                    help="the pipelines' load method: pull kernel, staged (copy-engine transfers into a "
+                         "workspace, then a scatter kernel on a third stream) or per-block copies; auto "
+                         "measures the first two and reports staged for compute-bound pipelines (a layer's "
+                         "compute at least its load), the pull kernel for copy-bound ones")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (reference for the traffic counters)")
     ap.add_argument("--decode-only", action="store_true",
@@ -928,9 +977,17 @@ def _main(args, sampler):
         pb = synth.l8b_pipe32()
         pst = measure_step(pb, args.steps, args.warmup)
         pld = measure_load(pb)
-        method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
-        print(json.dumps({"pipeline": measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"]),
-                          "load": pld, "step_ms": pst["step_ms"]}), flush=True)
+        lbp = _setup_pipeline(pb, pb.num_layers)
+        res = {}
+        for m in (("kernel_pull", "staged") if args.pipeline_method == "auto" else (args.pipeline_method,)):
+            if m == "staged":
+                sg = pld["dma_staged"]
+                res[m] = measure_pipeline(pb, m, sg["ms"], pst["step_ms"], staged_stages=(sg["transfer_ms"],
+                                                                                            sg["scatter_ms"]),
+                                          layers_bp=lbp)
+            else:
+                res[m] = measure_pipeline(pb, m, pld[m]["ms"], pst["step_ms"], layers_bp=lbp)
+        print(json.dumps({"pipeline": res, "load": pld, "step_ms": pst["step_ms"]}), flush=True)
         return 0
 
     batch = workload(args.workload)
@@ -946,7 +1003,8 @@ def _main(args, sampler):
         _say("[bench] clocks under the attention (amd-smi)")
         clocks = measure_clock_hold(batch, sampler)
 
-    method = "kernel_pull" if args.pipeline_method == "auto" else args.pipeline_method
+    method = "kernel_pull"
+    pipeline_methods = ("kernel_pull", "staged") if args.pipeline_method == "auto" else (args.pipeline_method,)
     load = None
     if not args.no_load:
         _say("[bench] load")
@@ -969,12 +1027,34 @@ def _main(args, sampler):
             _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, {distinct} distinct layer data sets)")
             pst = pst or measure_step(pb, 20, 3, min_warm_ms=200.0)
             pld = pld or measure_load(pb, reps=4)
-            rec = measure_pipeline(pb, args.pipeline_method, pld[method]["ms"], pst["step_ms"], reps=2,
-                                   distinct=distinct)
-            rec["attn_tflops"] = attention_flops(pb.prefix_lens, pb.suffix_lens, pb.num_q_heads,
-                                                 pb.head_dim) / (pst["attn_b2b_ms"] * 1e-3) / 1e12
-            rec["load_GBps"] = pld[method]["GBps"]
-            pipelines[pb.name] = rec
+            lbp = _setup_pipeline(pb, distinct)
+            recs = {}
+            for m in pipeline_methods:
+                if m == "staged":
+                    sg = pld["dma_staged"]
+                    rec = measure_pipeline(pb, "staged", sg["ms"], pst["step_ms"], reps=2, distinct=distinct,
+                                           staged_stages=(sg["transfer_ms"], sg["scatter_ms"]), layers_bp=lbp)
+                    rec["load_GBps"] = sg["GBps"]
+                else:
+                    rec = measure_pipeline(pb, m, pld[method]["ms"], pst["step_ms"], reps=2, distinct=distinct,
+                                           layers_bp=lbp)
+                    rec["load_GBps"] = pld[method]["GBps"]
+                rec["attn_tflops"] = attention_flops(pb.prefix_lens, pb.suffix_lens, pb.num_q_heads,
+                                                     pb.head_dim) / (pst["attn_b2b_ms"] * 1e-3) / 1e12
+                recs[m] = rec
+            del lbp
+            torch.cuda.synchronize()
+            # the pipeline's figure: the requested load method, or with "auto" the staged loads
+            # when a layer's compute is at least its load (compute-bound: the pull kernel's
+            # workgroups would slow the attention) and the pull kernel otherwise (copy-bound:
+            # the link sets the time, and the pull kernel adds no scatter); both are reported
+            if args.pipeline_method == "auto":
+                pick = "staged" if pst["step_ms"] >= pld[method]["ms"] else "kernel_pull"
+            else:
+                pick = args.pipeline_method
+            pipelines[pb.name] = dict(recs[pick], methods_measured={m: {k: r[k] for k in (
+                "total_ms", "bound_makespan_ms", "exposed_ms_per_layer", "exposed_frac_of_load",
+                "exposed_over_min_frac_of_load", "sum_compute_ms_in_pipeline")} for m, r in recs.items()})
             if pb.name == "l8b_pipe32_s6144":
                 _say(f"[bench] offload: {pb.name}")
                 off, osrc, odst = measure_offload(pb)

@@ -386,6 +386,37 @@ pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_layers, const 
                             float *timing_ms);
 
 /*
+ * pcr_pipeline_run_staged -- pcr_pipeline_run with every layer's load staged
+ * (Sec. 5: the layer's blocks go over the host link as batched copy-engine
+ * transfers on their own stream). Layer l's host blocks batch->src_blocks are
+ * moved by the copy engines into a workspace slot on copy_stream (one transfer
+ * per run of consecutive host blocks, K then V), then a kernel on scatter_stream
+ * writes them to pool blocks batch->dst_blocks; compute_stream waits for that
+ * scatter, then runs layer l's append and attention. The transfers hold no
+ * compute unit while attention runs beside them. workspace: device memory,
+ * 16-byte aligned, of workspace_bytes >= one slot = 2 * n_pairs * block_size *
+ * num_kv_heads * head_dim * 2 bytes (pcr_load_kv_layer_staged's workspace); it
+ * holds floor(workspace_bytes / slot) slots (at most n_layers), layer l using
+ * slot l mod slots, and the transfer into a slot waits for the scatter that last
+ * read it: with two or more slots, layer l+1's transfer runs while layer l is
+ * scattered. The workspace must not be used by other work until the pipeline has
+ * run; the first transfers wait for the work already queued on scatter_stream
+ * and compute_stream, and the first scatter for compute_stream. The three
+ * streams must differ (and overlap only on different hardware queues, as for
+ * pcr_pipeline_run). Every layer's pool must have the same block shape.
+ * timing_ms and errors as pcr_pipeline_run; [4l] (load ms) spans the layer's
+ * transfers and scatter. PCR_ERR_INVALID_ARG for a missing, misaligned or too
+ * small workspace or equal streams, before anything is queued.
+ * Choice of form: when a layer's compute takes at least as long as its load,
+ * this form leaves the attention its whole device and exposes less of the loads
+ * than pcr_pipeline_run's pull kernel; when the loads are longer (the host link
+ * sets the time) the pull kernel, which needs no scatter, is as fast or faster.
+ */
+pcr_status pcr_pipeline_run_staged(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
+                                   void *workspace, int64_t workspace_bytes, void *copy_stream,
+                                   void *scatter_stream, void *compute_stream, float *timing_ms);
+
+/*
  * pcr_pipeline_run_offload -- the three-stream form (Sec. 5: upload, compute and
  * download streams; Sec. 4.3: offloading a layer starts when its computation
  * ends). As pcr_pipeline_run, and in addition, after layer l's compute,

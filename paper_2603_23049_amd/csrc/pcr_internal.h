@@ -72,6 +72,20 @@ hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int3
 constexpr int64_t kDecodeScratchBytes = PCR_DECODE_NOALLOC_SCRATCH_BYTES;
 hipError_t decode_noalloc_scratch(void **ptr);
 
+// The staged host-to-pool load (every check of pcr_load_kv_layer_staged) with its two
+// halves on two streams: the copy-engine transfers into the workspace on dma_stream,
+// then dma_done is recorded there, scatter_stream waits for it and runs the scatter
+// into the pool. The workspace is free again once the scatter has run.
+pcr_status load_staged_split(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
+                             const int32_t *dst_blocks, int32_t n, void *workspace, int64_t workspace_bytes,
+                             hipStream_t dma_stream, hipStream_t scatter_stream, hipEvent_t dma_done);
+
+// Size in bytes of one pool block of K (or V): block_size * num_kv_heads * head_dim bf16.
+inline int64_t kv_block_bytes(int32_t block_size, int32_t num_kv_heads, int32_t head_dim)
+{
+    return (int64_t)block_size * num_kv_heads * head_dim * 2;
+}
+
 // Pool-to-host offload with any method (the staged one takes the workspace); used by
 // the pipeline, which chooses the method per call.
 pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,

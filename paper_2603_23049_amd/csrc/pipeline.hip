@@ -8,6 +8,13 @@
 // then copies the layer's new blocks to the host store. The copy stream first
 // waits for everything already queued on the compute (and offload) stream, so a
 // load never overwrites a pool that earlier work is still reading.
+//
+// The staged form splits each load in two: the copy engines move the layer's host
+// blocks into a workspace slot (copy stream), and a scatter kernel on a third
+// stream moves them from the slot into the pool. The host-link transfer then holds
+// no compute unit while the attention runs, and with two or more slots the transfer
+// of layer l+1 runs while layer l is scattered; the transfer into a slot waits for
+// the scatter that last read it.
 #include <algorithm>
 #include <vector>
 
@@ -53,17 +60,51 @@ using namespace pcr;
 
 namespace {
 
+// The staged loads' workspace and scatter stream (pcr_pipeline_run_staged).
+struct StagedLoads {
+    char *ws;
+    int64_t ws_bytes;
+    hipStream_t scatter;
+};
+
 pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_dst, int32_t n_layers,
                         const pcr_batch *batch, const int32_t *off_src, const int32_t *off_dst, int32_t n_off,
                         pcr_load_method method, pcr_load_method offload_method, void *workspace,
                         int64_t workspace_bytes, void *copy_stream, void *compute_stream, void *offload_stream,
-                        bool with_offload, float *timing_ms, const char *who)
+                        bool with_offload, const StagedLoads *staged, float *timing_ms, const char *who)
 {
     if (n_layers < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_layers < 0", who);
     if (n_layers == 0) return PCR_OK;
     if (!layers || !batch) return fail(PCR_ERR_INVALID_ARG, "%s: NULL layers or batch", who);
     if (copy_stream == compute_stream)
         return fail(PCR_ERR_INVALID_ARG, "%s: copy and compute streams must differ", who);
+    // staged loads: slots of one layer's K and V blocks each, in the caller's workspace
+    int64_t slot_bytes = 0;
+    int64_t n_slots = 0;
+    if (staged) {
+        if (staged->scatter == static_cast<hipStream_t>(copy_stream) ||
+            staged->scatter == static_cast<hipStream_t>(compute_stream))
+            return fail(PCR_ERR_INVALID_ARG, "%s: the scatter stream must differ from the other two", who);
+        if (batch->n_pairs < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_pairs < 0", who);
+        const pcr_kv_pool &p0 = layers[0].pool;
+        if (p0.block_size <= 0 || p0.num_kv_heads <= 0 || p0.head_dim <= 0)
+            return fail(PCR_ERR_INVALID_ARG, "%s: layer 0's pool has a non-positive shape", who);
+        for (int32_t l = 1; l < n_layers; ++l)
+            if (layers[l].pool.block_size != p0.block_size || layers[l].pool.num_kv_heads != p0.num_kv_heads ||
+                layers[l].pool.head_dim != p0.head_dim)
+                return fail(PCR_ERR_INVALID_ARG, "%s: layer %d's pool shape differs from layer 0's", who, l);
+        slot_bytes = 2 * (int64_t)batch->n_pairs * kv_block_bytes(p0.block_size, p0.num_kv_heads, p0.head_dim);
+        if (slot_bytes > 0) {
+            if (!staged->ws) return fail(PCR_ERR_INVALID_ARG, "%s: NULL workspace", who);
+            if ((uintptr_t)staged->ws & 15)
+                return fail(PCR_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+            n_slots = staged->ws_bytes / slot_bytes;
+            if (n_slots < 1)
+                return fail(PCR_ERR_INVALID_ARG, "%s: workspace of %lld bytes, one layer's load needs %lld", who,
+                            (long long)staged->ws_bytes, (long long)slot_bytes);
+            n_slots = std::min<int64_t>(n_slots, n_layers);
+        }
+    }
     if (with_offload) {
         if (offload_stream == compute_stream || offload_stream == copy_stream)
             return fail(PCR_ERR_INVALID_ARG, "%s: the offload stream must differ from the other two", who);
@@ -102,17 +143,19 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
     const bool timed = timing_ms != nullptr;
     const size_t n = (size_t)n_layers;
 
-    // events: [0] start, [1] offload-stream start, then per layer: load start, loaded,
-    // compute start, compute end, offload start, offload end (timed); loaded and
-    // compute end only (untimed)
+    // events: [0] start, [1] offload-stream start, [2] scatter-stream start, then per
+    // layer: load start, loaded, compute start, compute end, offload start, offload
+    // end, transfers done (timed); loaded, compute end, transfers done (untimed)
     EventPool &pool = timed ? g_timed_events : g_sync_events;
-    const size_t per = timed ? 6 : 2;
-    hipError_t e = pool.ensure(2 + per * n);
+    const size_t per = timed ? 7 : 3;
+    hipError_t e = pool.ensure(3 + per * n);
     if (e != hipSuccess) return hip_fail(e, "pcr_pipeline_run: hipEventCreate");
-    hipEvent_t ev_start = pool.ev[0], ev_ostart = pool.ev[1];
-    auto ev = [&](size_t l, int k) { return pool.ev[2 + per * l + k]; };
+    hipEvent_t ev_start = pool.ev[0], ev_ostart = pool.ev[1], ev_sstart = pool.ev[2];
+    auto ev = [&](size_t l, int k) { return pool.ev[3 + per * l + k]; };
     auto ev_loaded = [&](size_t l) { return ev(l, timed ? 1 : 0); };
     auto ev_cend = [&](size_t l) { return ev(l, timed ? 3 : 1); };
+    auto ev_dma = [&](size_t l) { return ev(l, timed ? 6 : 2); };
+    hipStream_t ss = staged ? staged->scatter : nullptr;
 
 #define PCR_HIP(call, what)                          \
     do {                                             \
@@ -126,16 +169,37 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
         PCR_HIP(hipEventRecord(ev_ostart, os), "pcr_pipeline_run: record offload start");
         PCR_HIP(hipStreamWaitEvent(cs, ev_ostart, 0), "pcr_pipeline_run: copy waits for offload");
     }
+    if (staged) {
+        // the first transfers wait for earlier scatters (which read the workspace), and
+        // the scatters for earlier compute (which reads the pools)
+        PCR_HIP(hipEventRecord(ev_sstart, ss), "pcr_pipeline_run: record scatter start");
+        PCR_HIP(hipStreamWaitEvent(cs, ev_sstart, 0), "pcr_pipeline_run: copy waits for scatter");
+        PCR_HIP(hipStreamWaitEvent(ss, ev_start, 0), "pcr_pipeline_run: scatter waits for compute");
+    }
     // One layer at a time: its load, then its compute (and offload). The streams run as
     // far ahead as their events allow either way; queuing a layer's compute right after
     // its load lets the compute stream start once the first load is done, not only after
     // the host has queued every load (about 0.2 ms each with the pull kernel).
     for (size_t l = 0; l < n; ++l) {
-        if (timed) PCR_HIP(hipEventRecord(ev(l, 0), cs), "pcr_pipeline_run: record load start");
-        pcr_status st = pcr_load_kv_layer_method(&layers[l].host, batch->src_blocks, &layers[l].pool,
-                                                 batch->dst_blocks, batch->n_pairs, method, copy_stream);
-        if (st) return st;
-        PCR_HIP(hipEventRecord(ev_loaded(l), cs), "pcr_pipeline_run: record loaded");
+        pcr_status st = PCR_OK;
+        if (staged) {
+            // slot l % n_slots was last read by the scatter of layer l - n_slots
+            if (l >= (size_t)n_slots && n_slots > 0)
+                PCR_HIP(hipStreamWaitEvent(cs, ev_loaded(l - (size_t)n_slots), 0),
+                        "pcr_pipeline_run: transfer waits for its slot");
+            if (timed) PCR_HIP(hipEventRecord(ev(l, 0), cs), "pcr_pipeline_run: record load start");
+            char *slot = n_slots > 0 ? staged->ws + (int64_t)(l % (size_t)n_slots) * slot_bytes : staged->ws;
+            st = load_staged_split(&layers[l].host, batch->src_blocks, &layers[l].pool, batch->dst_blocks,
+                                   batch->n_pairs, slot, slot_bytes, cs, ss, ev_dma(l));
+            if (st) return st;
+            PCR_HIP(hipEventRecord(ev_loaded(l), ss), "pcr_pipeline_run: record loaded");
+        } else {
+            if (timed) PCR_HIP(hipEventRecord(ev(l, 0), cs), "pcr_pipeline_run: record load start");
+            st = pcr_load_kv_layer_method(&layers[l].host, batch->src_blocks, &layers[l].pool, batch->dst_blocks,
+                                          batch->n_pairs, method, copy_stream);
+            if (st) return st;
+            PCR_HIP(hipEventRecord(ev_loaded(l), cs), "pcr_pipeline_run: record loaded");
+        }
         PCR_HIP(hipStreamWaitEvent(ks, ev_loaded(l), 0), "pcr_pipeline_run: compute waits for load");
         if (timed) PCR_HIP(hipEventRecord(ev(l, 2), ks), "pcr_pipeline_run: record compute start");
         st = pcr_append_kv(&layers[l].pool, layers[l].k_new, layers[l].v_new, batch->slot_mapping,
@@ -188,7 +252,17 @@ extern "C" pcr_status pcr_pipeline_run(const pcr_layer_io *layers, int32_t n_lay
                                        float *timing_ms)
 {
     return run_pipeline(layers, nullptr, n_layers, batch, nullptr, nullptr, 0, method, PCR_LOAD_AUTO, nullptr, 0,
-                        copy_stream, compute_stream, nullptr, false, timing_ms, "pcr_pipeline_run");
+                        copy_stream, compute_stream, nullptr, false, nullptr, timing_ms, "pcr_pipeline_run");
+}
+
+extern "C" pcr_status pcr_pipeline_run_staged(const pcr_layer_io *layers, int32_t n_layers, const pcr_batch *batch,
+                                              void *workspace, int64_t workspace_bytes, void *copy_stream,
+                                              void *scatter_stream, void *compute_stream, float *timing_ms)
+{
+    StagedLoads st{static_cast<char *>(workspace), workspace_bytes, static_cast<hipStream_t>(scatter_stream)};
+    return run_pipeline(layers, nullptr, n_layers, batch, nullptr, nullptr, 0, PCR_LOAD_DMA_STAGED, PCR_LOAD_AUTO,
+                        nullptr, 0, copy_stream, compute_stream, nullptr, false, &st, timing_ms,
+                        "pcr_pipeline_run_staged");
 }
 
 extern "C" pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_kv *offload_dst,
@@ -199,6 +273,6 @@ extern "C" pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const
                                                void *offload_stream, float *timing_ms)
 {
     return run_pipeline(layers, offload_dst, n_layers, batch, off_src, off_dst, n_off, method, offload_method,
-                        workspace, workspace_bytes, copy_stream, compute_stream, offload_stream, true, timing_ms,
-                        "pcr_pipeline_run_offload");
+                        workspace, workspace_bytes, copy_stream, compute_stream, offload_stream, true, nullptr,
+                        timing_ms, "pcr_pipeline_run_offload");
 }

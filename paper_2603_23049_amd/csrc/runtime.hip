@@ -58,7 +58,7 @@ pcr_status check_pool(const pcr_kv_pool *pool, const char *who)
     return PCR_OK;
 }
 
-int64_t block_bytes(int32_t block_size, int32_t Hkv, int32_t d) { return (int64_t)block_size * Hkv * d * 2; }
+int64_t block_bytes(int32_t block_size, int32_t Hkv, int32_t d) { return kv_block_bytes(block_size, Hkv, d); }
 
 // A host range is acceptable for the copy methods if HIP knows it as pinned host memory.
 pcr_status check_pinned(const void *ptr, int64_t bytes, const char *who, void **device_alias)
@@ -256,9 +256,12 @@ pcr_status staged_kernel(const pcr_kv_pool *pool, char *ws, const int32_t *pool_
     return PCR_OK;
 }
 
+// scatter_stream / dma_done: for the staged method only, optionally run the scatter on
+// a second stream: dma_done is recorded on copy_stream after the transfers, and the
+// scatter stream waits for it (the pipeline's staged form).
 pcr_status load_impl(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
                      const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *ws, int64_t ws_bytes,
-                     void *copy_stream)
+                     void *copy_stream, hipStream_t scatter_stream = nullptr, hipEvent_t dma_done = nullptr)
 {
     g_err[0] = 0;
     const char *who = "pcr_load_kv_layer";
@@ -311,6 +314,12 @@ pcr_status load_impl(const pcr_host_kv *src, const int32_t *src_blocks, const pc
         st = staged_dma(const_cast<char *>(hk), const_cast<char *>(hv), static_cast<char *>(ws), src_blocks, n, bb,
                         false, s, "pcr_load_kv_layer: hipMemcpyAsync");
         if (st) return st;
+        if (dma_done) {
+            hipError_t e = hipEventRecord(dma_done, s);
+            if (e == hipSuccess) e = hipStreamWaitEvent(scatter_stream, dma_done, 0);
+            if (e != hipSuccess) return hip_fail(e, "pcr_load_kv_layer: scatter stream waits for the transfers");
+            s = scatter_stream;
+        }
         return staged_kernel(dst, static_cast<char *>(ws), dst_blocks, n, bb, false, s,
                              "pcr_load_kv_layer: scatter kernel launch");
     }
@@ -814,6 +823,14 @@ pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, i
 }  // extern "C"
 
 namespace pcr {
+
+pcr_status load_staged_split(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
+                             const int32_t *dst_blocks, int32_t n, void *workspace, int64_t workspace_bytes,
+                             hipStream_t dma_stream, hipStream_t scatter_stream, hipEvent_t dma_done)
+{
+    return load_impl(src, src_blocks, dst, dst_blocks, n, PCR_LOAD_DMA_STAGED, workspace, workspace_bytes,
+                     dma_stream, scatter_stream, dma_done);
+}
 
 pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const pcr_host_kv *dst,
                         const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *workspace,

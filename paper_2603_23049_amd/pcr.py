@@ -35,7 +35,8 @@ LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block":
 EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_layer_method",
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
-           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_offload",
+           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_staged",
+           "pcr_pipeline_run_offload",
            "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
            "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
 
@@ -97,6 +98,8 @@ def lib():
         L.pcr_gather_kv.argtypes = [ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, P, P, P]
         L.pcr_pipeline_run.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), ctypes.c_int, P, P,
                                        P]
+        L.pcr_pipeline_run_staged.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), P, i64, P, P,
+                                              P, P]
         L.pcr_plan_offload.argtypes = [i32, P, P, P, i32, i32, i32, i32, P, P, i32, P]
         L.pcr_offload_kv_layer.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32, P]
         L.pcr_offload_kv_layer_method.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32,
@@ -411,6 +414,34 @@ def pipeline_run(layers: Sequence[Layer], batch: BatchPlan, copy_stream, compute
     per = t[:4 * n].reshape(n, 4)
     return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
             "end_ms": per[:, 3].copy(), "total_ms": float(t[4 * n]), "sum_compute_ms": float(t[4 * n + 1])}
+
+
+def pipeline_run_staged(layers: Sequence[Layer], batch: BatchPlan, workspace, copy_stream, scatter_stream,
+                        compute_stream, timing: bool = False):
+    """pcr_pipeline_run_staged: loads as copy-engine transfers into `workspace` slots
+    (copy stream) and a scatter into the pool (scatter stream). `workspace`: a device
+    tensor of at least one slot, pipeline_staged_slot_bytes(...) bytes; whole slots
+    beyond the first let the next transfer run during a scatter. Timing as
+    pipeline_run."""
+    n = len(layers)
+    arr = (_LayerIO * max(n, 1))()
+    for i, L in enumerate(layers):
+        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    b = batch.c()
+    t = np.zeros(4 * n + 2, np.float32) if timing else None
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(lib().pcr_pipeline_run_staged(arr, n, ctypes.byref(b), _ptr(workspace), ws_bytes, _stream(copy_stream),
+                                         _stream(scatter_stream), _stream(compute_stream), _ptr(t)))
+    if not timing:
+        return None
+    per = t[:4 * n].reshape(n, 4)
+    return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
+            "end_ms": per[:, 3].copy(), "total_ms": float(t[4 * n]), "sum_compute_ms": float(t[4 * n + 1])}
+
+
+def pipeline_staged_slot_bytes(n_pairs: int, num_kv_heads: int, head_dim: int, block_size: int = 16) -> int:
+    """One slot of pcr_pipeline_run_staged's workspace: one layer's loaded K and V blocks."""
+    return staged_workspace_bytes(n_pairs, num_kv_heads, head_dim, block_size)
 
 
 def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV], batch: BatchPlan, off_src, off_dst,

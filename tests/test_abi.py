@@ -178,6 +178,27 @@ def test_argument_validation_before_any_device_work():
     bat2.num_q_heads = 3
     assert L.pcr_pipeline_run_offload(lay2, None, 2, P(bat2), None, None, 0, 0, 0, None, 0, 0x5, 0x6, 0x7,
                                       None) == pcr.PCR_ERR_UNSUPPORTED
+    # staged pipeline: streams, workspace and pool shapes are checked before anything is queued
+    slot = 2 * 3 * 16 * 2 * 64 * 2        # 3 pairs of (16-token, 2-head, d=64) K and V blocks
+    bat2.n_pairs = 3
+    assert L.pcr_pipeline_run_staged(None, 0, None, None, 0, None, None, None, None) == pcr.PCR_OK
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x5, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG and "scatter stream" in pcr.last_error()
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x6, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), None, slot, 0x5, 0x7, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG and "NULL workspace" in pcr.last_error()
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1008, slot, 0x5, 0x7, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG and "aligned" in pcr.last_error()
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot - 16, 0x5, 0x7, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG and f"needs {slot}" in pcr.last_error()
+    lay2[1].pool = _pool(Hkv=1, k=0x110000, v=0x120000)
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x7, 0x6, None) == \
+        pcr.PCR_ERR_INVALID_ARG and "shape differs" in pcr.last_error()
+    lay2[1].pool = _pool(Hkv=2, k=0x110000, v=0x120000)
+    # valid workspace: the attention checks come next (three q heads over two kv heads)
+    assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x7, 0x6, None) == \
+        pcr.PCR_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("mk", [synth.tiny, synth.l8b_layer, synth.l70b_pipe80])

@@ -71,6 +71,75 @@ def test_pipeline_equals_serial_bitwise(method):
     assert mx <= MAX_ABS and mean <= MEAN_ABS
 
 
+@pytest.mark.parametrize("slots", [1, 2, 3, 9])
+def test_staged_pipeline_equals_serial_bitwise(slots):
+    """Loads as copy-engine transfers into workspace slots and a scatter on a third
+    stream: with one slot every transfer waits for the previous scatter, with more the
+    transfers run ahead (9 slots for 6 layers: each layer its own). Pools poisoned with
+    NaN bit patterns, the copy and the scatter streams each delayed by a large unrelated
+    copy queued first: every output must equal the serialized one bit for bit."""
+    n = 6
+    b = synth.uniform_batch("pipe", B=2, Hq=32, Hkv=8, d=128, p=1024, s=200, pool_blocks=512, seed=3,
+                            num_layers=n, layer_seed_base=3000)
+    say(f"[gpu] staged pipeline {n} layers, {slots} workspace slots")
+    layers, poison = _layers(b, n)
+    serial = []
+    for L in layers:
+        L.run_serial("kernel_pull")
+        serial.append(u16(L.out).copy())
+        L.pool.k.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.pool.v.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.out.zero_()
+    torch.cuda.synchronize()
+    bp = layers[0].batch_plan()
+    slot = pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), b.num_kv_heads, b.head_dim)
+    ws = torch.empty(slots * slot + 8, dtype=torch.uint8, device="cuda")   # a partial slot beyond is unused
+    copy_s, scat_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    big_h = pinned(np.ones(64 << 20, np.uint8))
+    big_d = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    big_d2 = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(copy_s):
+        big_d.copy_(big_h, non_blocking=True)
+    with torch.cuda.stream(scat_s):
+        big_d2.fill_(3)
+        big_d2.add_(1)
+    timing = pcr.pipeline_run_staged([L.layer_io() for L in layers], bp, ws, copy_s, scat_s, comp_s, timing=True)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        got = u16(L.out)
+        assert not np.any((got & 0x7F80) == 0x7F80), f"layer {l}: non-finite output (missing wait)"
+        assert np.array_equal(got, serial[l]), f"layer {l}: staged pipeline differs from serial"
+    assert timing["total_ms"] > 0 and np.all(timing["load_ms"] > 0) and np.all(timing["compute_ms"] > 0)
+
+
+def test_staged_pipeline_twice_on_one_workspace():
+    """Two staged pipelines queued back to back on the same workspace and streams, the
+    second over other layers: the second call's first transfers wait for the first
+    call's scatters (which read the slots), so both give the serialized outputs."""
+    n = 4
+    b = synth.uniform_batch("pipe2", B=2, Hq=16, Hkv=4, d=128, p=700, s=90, pool_blocks=160, seed=5,
+                            num_layers=2 * n, layer_seed_base=5000)
+    layers, poison = _layers(b, 2 * n)
+    serial = []
+    for L in layers:
+        L.run_serial("kernel_pull")
+        serial.append(u16(L.out).copy())
+        L.pool.k.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.pool.v.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.out.zero_()
+    torch.cuda.synchronize()
+    bp = layers[0].batch_plan()
+    ws = torch.empty(pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), b.num_kv_heads, b.head_dim) * 2,
+                     dtype=torch.uint8, device="cuda")
+    copy_s, scat_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    say("[gpu] two staged pipelines on one workspace")
+    pcr.pipeline_run_staged([L.layer_io() for L in layers[:n]], bp, ws, copy_s, scat_s, comp_s)
+    pcr.pipeline_run_staged([L.layer_io() for L in layers[n:]], bp, ws, copy_s, scat_s, comp_s)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        assert np.array_equal(u16(L.out), serial[l]), f"layer {l}"
+
+
 def test_pipeline_partial_prefix_block_ordering():
     """p % 16 != 0: the last cached block is loaded whole and then partly
     overwritten by the append; the pipeline must keep that order per layer."""
@@ -109,8 +178,8 @@ def _special_layers(n):
 
 
 def _full_pipeline(name):
-    """Runs the named pipeline once per test session (method "auto", every pool poisoned
-    with NaN bit patterns beforehand) and checks, for every layer, that its pool is the
+    """Runs the named pipeline once per test session with method "auto", then again with
+    staged loads (every pool poisoned with NaN bit patterns before each run) and checks, for every layer, that its pool is the
     oracle's bit for bit and its output equals its data set's serialized result bit for
     bit. Keeps, for the first, middle and last layers, the output and the oracle's inputs."""
     if name in _FULL_RESULTS:
@@ -140,28 +209,46 @@ def _full_pipeline(name):
                           b.head_dim)
         ios.append(pcr.Layer(src.host, pool, src.q, src.k_new, src.v_new, torch.zeros_like(src.out)))
     torch.cuda.synchronize()
-    say(f"    running the pipeline")
-    copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
-    pcr.pipeline_run(ios, base[0].batch_plan(), copy_s, comp_s, method="auto")
-    torch.cuda.synchronize()
     plan = odm.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, BS)
     special = _special_layers(n)
     keep = {}
-    for k in range(n_sets):
-        data = datas[k]
-        pk, pv = odm.pool_after_layer(poison, poison, data.host_k, data.host_v, plan, data.k_new, data.v_new, BS)
-        pk_d = torch.from_numpy(pk.view(np.int16)).cuda()
-        pv_d = torch.from_numpy(pv.view(np.int16)).cuda()
-        for l in range(n):
-            if sets[l] != k:
-                continue
-            io = ios[l]
-            assert torch.equal(io.pool.k, pk_d) and torch.equal(io.pool.v, pv_d), f"layer {l}: pool differs"
-            assert torch.equal(io.out, serial[k]), f"layer {l}: pipeline output differs from serial"
-            if l in special:
-                keep[l] = {"out": u16(io.out), "q": data.q, "pk": pk, "pv": pv}
-        del pk_d, pv_d
-    say(f"    every layer's pool equals the oracle's and every output the serial result, bit for bit")
+    oracle_pools = [None] * n_sets
+    bp = base[0].batch_plan()
+    copy_s, scat_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    ws = torch.empty(2 * pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), b.num_kv_heads, b.head_dim),
+                     dtype=torch.uint8, device="cuda")
+    for form in ("auto", "staged"):
+        say(f"    running the pipeline ({form} loads)")
+        if form == "auto":
+            pcr.pipeline_run(ios, bp, copy_s, comp_s, method="auto")
+        else:
+            for io in ios:
+                io.pool.k.fill_(int(NAN_BITS))
+                io.pool.v.fill_(int(NAN_BITS))
+                io.out.zero_()
+            torch.cuda.synchronize()
+            pcr.pipeline_run_staged(ios, bp, ws, copy_s, scat_s, comp_s)
+        torch.cuda.synchronize()
+        for k in range(n_sets):
+            data = datas[k]
+            if oracle_pools[k] is None:
+                oracle_pools[k] = odm.pool_after_layer(poison, poison, data.host_k, data.host_v, plan, data.k_new,
+                                                       data.v_new, BS)
+            pk, pv = oracle_pools[k]
+            pk_d = torch.from_numpy(pk.view(np.int16)).cuda()
+            pv_d = torch.from_numpy(pv.view(np.int16)).cuda()
+            for l in range(n):
+                if sets[l] != k:
+                    continue
+                io = ios[l]
+                assert torch.equal(io.pool.k, pk_d) and torch.equal(io.pool.v, pv_d), \
+                    f"layer {l}: pool differs ({form})"
+                assert torch.equal(io.out, serial[k]), f"layer {l}: pipeline output differs from serial ({form})"
+                if l in special and form == "auto":
+                    keep[l] = {"out": u16(io.out), "q": data.q, "pk": pk, "pv": pv}
+            del pk_d, pv_d
+        say(f"    every layer's pool equals the oracle's and every output the serial result, bit for bit")
+    del ws, oracle_pools
     res = {"batch": b, "plan": plan, "layers": keep}
     del ios, base, serial
     torch.cuda.synchronize()
@@ -172,9 +259,10 @@ def _full_pipeline(name):
 
 @pytest.mark.parametrize("name", list(FULL))
 def test_pipeline_full_size(name):
-    """The benchmark's three pipelines at full size: every layer's pool after the
-    pipeline is the oracle's bit for bit, every output equals its data set's serialized
-    result bit for bit."""
+    """The benchmark's three pipelines at full size, with pull-kernel loads and with
+    staged loads (two workspace slots): every layer's pool after the pipeline is the
+    oracle's bit for bit, every output equals its data set's serialized result bit for
+    bit."""
     res = _full_pipeline(name)
     assert set(res["layers"]) == set(_special_layers(res["batch"].num_layers))
 
