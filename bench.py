@@ -915,8 +915,12 @@ def main(argv=None):
     ap.add_argument("--append-sweep-only", action="store_true",
                     help="only run the append (scatter) sweep and print its JSON")
     ap.add_argument("--pipeline-only", action="store_true",
-                    help="only run the 32-layer pipeline (with its isolated load and compute times) and print "
-                         "its JSON")
+                    help="only run one pipeline (--pipeline-workload) with its isolated load and compute times, "
+                         "per load method, and print its JSON")
+    ap.add_argument("--pipeline-workload", default="l8b_pipe32",
+                    choices=("l8b_pipe32", "l8b_pipe32_s6144", "l70b_pipe80"))
+    ap.add_argument("--pipeline-reps", type=int, default=3,
+                    help="with --pipeline-only: untimed pipeline runs per load method after one warm-up run")
     ap.add_argument("--no-clocks", action="store_true",
                     help="skip the amd-smi clock samples under the attention (never taken under a profiler)")
     args = ap.parse_args(argv)
@@ -974,19 +978,21 @@ def _main(args, sampler):
         print(json.dumps({"append_sweep": measure_append_sweep()}), flush=True)
         return 0
     if args.pipeline_only:
-        pb = synth.l8b_pipe32()
+        pb = workload(args.pipeline_workload)
         pst = measure_step(pb, args.steps, args.warmup)
         pld = measure_load(pb)
-        lbp = _setup_pipeline(pb, pb.num_layers)
+        dist = pb.num_layers if pb.name == "l8b_pipe32" else 6
+        lbp = _setup_pipeline(pb, dist)
         res = {}
         for m in (("kernel_pull", "staged") if args.pipeline_method == "auto" else (args.pipeline_method,)):
             if m == "staged":
                 sg = pld["dma_staged"]
                 res[m] = measure_pipeline(pb, m, sg["ms"], pst["step_ms"], staged_stages=(sg["transfer_ms"],
                                                                                             sg["scatter_ms"]),
-                                          layers_bp=lbp)
+                                          reps=args.pipeline_reps, distinct=dist, layers_bp=lbp)
             else:
-                res[m] = measure_pipeline(pb, m, pld[m]["ms"], pst["step_ms"], layers_bp=lbp)
+                res[m] = measure_pipeline(pb, m, pld[m]["ms"], pst["step_ms"], reps=args.pipeline_reps, distinct=dist,
+                                          layers_bp=lbp)
         print(json.dumps({"pipeline": res, "load": pld, "step_ms": pst["step_ms"]}), flush=True)
         return 0
 
