@@ -676,10 +676,12 @@ def measure_offload(batch, reps=6, chunk=256):
 
 
 def measure_pipeline_offload(batch, method, load_ms_iso, compute_ms_iso, offload_ms_iso, src, dst, reps=2,
-                             distinct=4, offload_method="dma_staged"):
-    """The three-stream pipeline (load, compute, offload of the computed chunks).
+                             distinct=4, offload_method="dma_staged", staged_stages=None):
+    """The three-stream pipeline (load, compute, offload of the computed chunks), or with
+    method "staged" the four-stream one (transfers, scatter, compute, offload).
     Exposure per layer = (pipeline time - n x isolated compute) / n; its least value
-    follows from the isolated per-layer times of the three steps."""
+    follows from the isolated per-layer times of the steps (staged_stages = (transfer
+    ms, scatter ms) for the staged loads)."""
     import torch
     from paper_2603_23049_amd import pcr
     n = batch.num_layers
@@ -689,13 +691,25 @@ def measure_pipeline_offload(batch, method, load_ms_iso, compute_ms_iso, offload
     cs, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     ws = torch.empty(pcr.staged_workspace_bytes(len(src), batch.num_kv_heads, batch.head_dim), dtype=torch.uint8,
                      device="cuda")
-    total = _bracketed_ms(lambda: pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
-                                                           offload_method=offload_method, workspace=ws),
-                          ks, os_, reps)
-    best = pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
-                                    offload_method=offload_method, workspace=ws, timing=True)
+    if method == "staged":
+        ss = torch.cuda.Stream()
+        lws = torch.empty(2 * pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), batch.num_kv_heads, batch.head_dim),
+                          dtype=torch.uint8, device="cuda")
+        run = lambda timing=False: pcr.pipeline_run_offload_staged(layers, dsts, bp, src, dst, lws, cs, ss, ks, os_,
+                                                                   offload_method=offload_method,
+                                                                   offload_workspace=ws, timing=timing)
+    else:
+        run = lambda timing=False: pcr.pipeline_run_offload(layers, dsts, bp, src, dst, cs, ks, os_, method=method,
+                                                            offload_method=offload_method, workspace=ws,
+                                                            timing=timing)
+    total = _bracketed_ms(lambda: run(), ks, os_, reps)
+    best = run(timing=True)
     e_raw = total / n - compute_ms_iso
-    bound = flow_shop3_makespan(load_ms_iso, compute_ms_iso, offload_ms_iso, n)
+    if method == "staged":
+        stages = (staged_stages[0], staged_stages[1], compute_ms_iso, offload_ms_iso)
+        bound = sum(stages) + (n - 1) * max(stages)
+    else:
+        bound = flow_shop3_makespan(load_ms_iso, compute_ms_iso, offload_ms_iso, n)
     e_min = bound / n - compute_ms_iso
     del layers, outs, dsts
     torch.cuda.synchronize()
@@ -1070,6 +1084,11 @@ def _main(args, sampler):
                     pipelines[f"{pb.name}_offload_{key}"] = measure_pipeline_offload(
                         pb, method, pld[method]["ms"], pst["step_ms"], off[key]["ms"], osrc, odst,
                         offload_method=om, distinct=6)
+                _say(f"[bench] pipeline with staged loads and offload (dma_staged): {pb.name}")
+                sg = pld["dma_staged"]
+                pipelines[f"{pb.name}_staged_offload_dma_staged"] = measure_pipeline_offload(
+                    pb, "staged", sg["ms"], pst["step_ms"], off["dma_staged"]["ms"], osrc, odst,
+                    offload_method="dma_staged", distinct=6, staged_stages=(sg["transfer_ms"], sg["scatter_ms"]))
     if not args.no_extra:
         _say("[bench] SSD tier: queue-window prefetch")
         extra["prefetch"] = measure_prefetch()

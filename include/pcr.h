@@ -443,6 +443,27 @@ pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_k
                                     float *timing_ms);
 
 /*
+ * pcr_pipeline_run_offload_staged -- pcr_pipeline_run_offload with the loads
+ * staged as in pcr_pipeline_run_staged: four streams (copy-engine transfers into
+ * load_workspace slots on copy_stream, the scatter into the pool on
+ * scatter_stream, append and attention on compute_stream, the offload of layer l
+ * after its compute on offload_stream with offload_method and offload_workspace).
+ * load_workspace follows pcr_pipeline_run_staged's workspace rules;
+ * offload_workspace pcr_pipeline_run_offload's; the two must not overlap. Besides
+ * the waits of both forms, the first scatter also waits for the work already
+ * queued on offload_stream (an earlier offload may still read a pool). The four
+ * streams must differ. timing_ms and errors as pcr_pipeline_run_offload; [6l]
+ * (load ms) spans the layer's transfers and scatter.
+ */
+pcr_status pcr_pipeline_run_offload_staged(const pcr_layer_io *layers, const pcr_host_kv *offload_dst,
+                                           int32_t n_layers, const pcr_batch *batch, const int32_t *off_src,
+                                           const int32_t *off_dst, int32_t n_off, pcr_load_method offload_method,
+                                           void *offload_workspace, int64_t offload_workspace_bytes,
+                                           void *load_workspace, int64_t load_workspace_bytes, void *copy_stream,
+                                           void *scatter_stream, void *compute_stream, void *offload_stream,
+                                           float *timing_ms);
+
+/*
  * The SSD tier of the chunk cache (Sec. 4.4 queue-based prefetch and asynchronous
  * write-back; Sec. 5 dedicated prefetch thread). A store is one file of fixed-size
  * chunk slots (chunk id c at byte c * chunk_bytes) served by io_threads host

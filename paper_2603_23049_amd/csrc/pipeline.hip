@@ -111,6 +111,8 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
         if (n_off < 0) return fail(PCR_ERR_INVALID_ARG, "%s: n_off < 0", who);
         if (n_off > 0 && (!offload_dst || !off_src || !off_dst))
             return fail(PCR_ERR_INVALID_ARG, "%s: NULL offload argument", who);
+        if (staged && staged->scatter == static_cast<hipStream_t>(offload_stream))
+            return fail(PCR_ERR_INVALID_ARG, "%s: the scatter and offload streams must differ", who);
     }
     // Every layer needs a pool of its own: nothing orders layer l+1's load (copy stream)
     // after layer l's compute (compute stream), so two layers sharing pool memory would
@@ -175,6 +177,8 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
         PCR_HIP(hipEventRecord(ev_sstart, ss), "pcr_pipeline_run: record scatter start");
         PCR_HIP(hipStreamWaitEvent(cs, ev_sstart, 0), "pcr_pipeline_run: copy waits for scatter");
         PCR_HIP(hipStreamWaitEvent(ss, ev_start, 0), "pcr_pipeline_run: scatter waits for compute");
+        if (with_offload)   // the scatters write pools that earlier offloads may still read
+            PCR_HIP(hipStreamWaitEvent(ss, ev_ostart, 0), "pcr_pipeline_run: scatter waits for offload");
     }
     // One layer at a time: its load, then its compute (and offload). The streams run as
     // far ahead as their events allow either way; queuing a layer's compute right after
@@ -263,6 +267,19 @@ extern "C" pcr_status pcr_pipeline_run_staged(const pcr_layer_io *layers, int32_
     return run_pipeline(layers, nullptr, n_layers, batch, nullptr, nullptr, 0, PCR_LOAD_DMA_STAGED, PCR_LOAD_AUTO,
                         nullptr, 0, copy_stream, compute_stream, nullptr, false, &st, timing_ms,
                         "pcr_pipeline_run_staged");
+}
+
+extern "C" pcr_status pcr_pipeline_run_offload_staged(
+    const pcr_layer_io *layers, const pcr_host_kv *offload_dst, int32_t n_layers, const pcr_batch *batch,
+    const int32_t *off_src, const int32_t *off_dst, int32_t n_off, pcr_load_method offload_method,
+    void *offload_workspace, int64_t offload_workspace_bytes, void *load_workspace, int64_t load_workspace_bytes,
+    void *copy_stream, void *scatter_stream, void *compute_stream, void *offload_stream, float *timing_ms)
+{
+    StagedLoads st{static_cast<char *>(load_workspace), load_workspace_bytes,
+                   static_cast<hipStream_t>(scatter_stream)};
+    return run_pipeline(layers, offload_dst, n_layers, batch, off_src, off_dst, n_off, PCR_LOAD_DMA_STAGED,
+                        offload_method, offload_workspace, offload_workspace_bytes, copy_stream, compute_stream,
+                        offload_stream, true, &st, timing_ms, "pcr_pipeline_run_offload_staged");
 }
 
 extern "C" pcr_status pcr_pipeline_run_offload(const pcr_layer_io *layers, const pcr_host_kv *offload_dst,

@@ -36,7 +36,7 @@ EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_lay
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
            "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_staged",
-           "pcr_pipeline_run_offload",
+           "pcr_pipeline_run_offload", "pcr_pipeline_run_offload_staged",
            "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
            "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
 
@@ -100,6 +100,9 @@ def lib():
                                        P]
         L.pcr_pipeline_run_staged.argtypes = [ctypes.POINTER(_LayerIO), i32, ctypes.POINTER(_Batch), P, i64, P, P,
                                               P, P]
+        L.pcr_pipeline_run_offload_staged.argtypes = [ctypes.POINTER(_LayerIO), ctypes.POINTER(_Host), i32,
+                                                      ctypes.POINTER(_Batch), P, P, i32, ctypes.c_int, P, i64, P,
+                                                      i64, P, P, P, P, P]
         L.pcr_plan_offload.argtypes = [i32, P, P, P, i32, i32, i32, i32, P, P, i32, P]
         L.pcr_offload_kv_layer.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32, P]
         L.pcr_offload_kv_layer_method.argtypes = [ctypes.POINTER(_Pool), P, ctypes.POINTER(_Host), P, i32,
@@ -444,11 +447,7 @@ def pipeline_staged_slot_bytes(n_pairs: int, num_kv_heads: int, head_dim: int, b
     return staged_workspace_bytes(n_pairs, num_kv_heads, head_dim, block_size)
 
 
-def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV], batch: BatchPlan, off_src, off_dst,
-                         copy_stream, compute_stream, offload_stream, method: str = "auto",
-                         offload_method: str = "auto", workspace=None, timing: bool = False):
-    """pcr_pipeline_run_offload: the three-stream pipeline. With timing=True, waits for the
-    last offload and returns per-layer load/compute/wait/offload ms and totals."""
+def _offload_args(layers, offload_dst, off_src, off_dst):
     n = len(layers)
     if len(offload_dst) != n:
         raise ValueError("one offload destination per layer")
@@ -461,19 +460,51 @@ def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV],
     sb, db = _i32_host(off_src), _i32_host(off_dst)
     if sb.shape != db.shape:
         raise ValueError("off_src and off_dst differ in length")
-    b = batch.c()
-    t = np.zeros(6 * n + 3, np.float32) if timing else None
-    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
-    _check(lib().pcr_pipeline_run_offload(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
-                                          LOAD_METHODS[method], LOAD_METHODS[offload_method], _ptr(workspace),
-                                          ws_bytes, _stream(copy_stream), _stream(compute_stream),
-                                          _stream(offload_stream), _ptr(t)))
-    if not timing:
-        return None
+    return n, arr, dst, sb, db
+
+
+def _offload_timing(t, n):
     per = t[:6 * n].reshape(n, 6)
     return {"load_ms": per[:, 0].copy(), "compute_ms": per[:, 1].copy(), "wait_ms": per[:, 2].copy(),
             "end_ms": per[:, 3].copy(), "offload_ms": per[:, 4].copy(), "offload_end_ms": per[:, 5].copy(),
             "total_ms": float(t[6 * n]), "sum_compute_ms": float(t[6 * n + 1]), "compute_end_ms": float(t[6 * n + 2])}
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else int(t.numel() * t.element_size())
+
+
+def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV], batch: BatchPlan, off_src, off_dst,
+                         copy_stream, compute_stream, offload_stream, method: str = "auto",
+                         offload_method: str = "auto", workspace=None, timing: bool = False):
+    """pcr_pipeline_run_offload: the three-stream pipeline. With timing=True, waits for the
+    last offload and returns per-layer load/compute/wait/offload ms and totals."""
+    n, arr, dst, sb, db = _offload_args(layers, offload_dst, off_src, off_dst)
+    b = batch.c()
+    t = np.zeros(6 * n + 3, np.float32) if timing else None
+    _check(lib().pcr_pipeline_run_offload(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
+                                          LOAD_METHODS[method], LOAD_METHODS[offload_method], _ptr(workspace),
+                                          _nbytes(workspace), _stream(copy_stream), _stream(compute_stream),
+                                          _stream(offload_stream), _ptr(t)))
+    return _offload_timing(t, n) if timing else None
+
+
+def pipeline_run_offload_staged(layers: Sequence[Layer], offload_dst: Sequence[HostKV], batch: BatchPlan, off_src,
+                                off_dst, load_workspace, copy_stream, scatter_stream, compute_stream, offload_stream,
+                                offload_method: str = "auto", offload_workspace=None, timing: bool = False):
+    """pcr_pipeline_run_offload_staged: the offload pipeline with staged loads (four
+    streams). load_workspace as pipeline_run_staged's workspace; offload_workspace as
+    pipeline_run_offload's. Timing as pipeline_run_offload."""
+    n, arr, dst, sb, db = _offload_args(layers, offload_dst, off_src, off_dst)
+    b = batch.c()
+    t = np.zeros(6 * n + 3, np.float32) if timing else None
+    _check(lib().pcr_pipeline_run_offload_staged(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
+                                                 LOAD_METHODS[offload_method], _ptr(offload_workspace),
+                                                 _nbytes(offload_workspace), _ptr(load_workspace),
+                                                 _nbytes(load_workspace), _stream(copy_stream),
+                                                 _stream(scatter_stream), _stream(compute_stream),
+                                                 _stream(offload_stream), _ptr(t)))
+    return _offload_timing(t, n) if timing else None
 
 
 class ChunkStore:

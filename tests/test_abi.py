@@ -196,6 +196,12 @@ def test_argument_validation_before_any_device_work():
     assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x7, 0x6, None) == \
         pcr.PCR_ERR_INVALID_ARG and "shape differs" in pcr.last_error()
     lay2[1].pool = _pool(Hkv=2, k=0x110000, v=0x120000)
+    # the four-stream form also needs the scatter and offload streams apart
+    assert L.pcr_pipeline_run_offload_staged(lay2, None, 2, P(bat2), None, None, 0, 0, None, 0, 0x1000, slot, 0x5,
+                                             0x7, 0x6, 0x7, None) == pcr.PCR_ERR_INVALID_ARG
+    assert "scatter stream must differ" in pcr.last_error() or "offload stream" in pcr.last_error()
+    assert L.pcr_pipeline_run_offload_staged(lay2, None, 2, P(bat2), None, None, 0, 0, None, 0, 0x1000, slot, 0x5,
+                                             0x8, 0x6, 0x7, None) == pcr.PCR_ERR_UNSUPPORTED
     # valid workspace: the attention checks come next (three q heads over two kv heads)
     assert L.pcr_pipeline_run_staged(lay2, 2, P(bat2), 0x1000, slot, 0x5, 0x7, 0x6, None) == \
         pcr.PCR_ERR_UNSUPPORTED

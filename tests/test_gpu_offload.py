@@ -127,6 +127,54 @@ def test_pipeline_with_offload_bitwise(method):
     assert np.all(t["offload_end_ms"][1:] >= t["offload_end_ms"][:-1])
 
 
+@pytest.mark.parametrize("offload_method", ["dma_staged", "kernel_pull"])
+def test_pipeline_with_offload_staged_loads_bitwise(offload_method):
+    """Four streams: staged loads (transfers, then a scatter on its own stream), compute,
+    offload. Pools poisoned with NaN bit patterns, the scatter and offload streams each
+    delayed by unrelated device work queued first: outputs equal the serialized ones
+    and every offloaded block the oracle's, bit for bit."""
+    n = 5
+    b = synth.uniform_batch("pipe_off_stg", B=2, Hq=32, Hkv=8, d=128, p=1024, s=520, pool_blocks=512, seed=4,
+                            num_layers=n, layer_seed_base=3200)
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    poison = np.full(shape, NAN_BITS, np.uint16)
+    layers = [GpuLayer(b, synth.make_layer(b, l), poison, poison) for l in range(n)]
+    src, dst = pcr.plan_offload(b.prefix_lens, b.suffix_lens, b.block_tables, BS, 256)
+    n_blocks = len(src)
+    outs = [_host_out(b, n_blocks) for _ in range(n)]
+    say(f"[gpu] pipeline with staged loads and offload ({offload_method}), {n} layers")
+    serial = []
+    for L in layers:
+        L.run_serial("kernel_pull")
+        serial.append(u16(L.out).copy())
+        L.pool.k.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.pool.v.copy_(torch.from_numpy(poison.view(np.int16)))
+        L.out.zero_()
+    torch.cuda.synchronize()
+    bp = layers[0].batch_plan()
+    ows = torch.empty(pcr.staged_workspace_bytes(len(src), b.num_kv_heads, b.head_dim), dtype=torch.uint8,
+                      device="cuda")
+    lws = torch.empty(2 * pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), b.num_kv_heads, b.head_dim),
+                      dtype=torch.uint8, device="cuda")
+    cs, ss, ks, os_ = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    junk = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+    for st_ in (ss, os_):
+        with torch.cuda.stream(st_):
+            junk.fill_(7)
+            junk.add_(1)
+    t = pcr.pipeline_run_offload_staged([L.layer_io() for L in layers], outs, bp, src, dst, lws, cs, ss, ks, os_,
+                                        offload_method=offload_method, offload_workspace=ows, timing=True)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        got = u16(L.out)
+        assert not np.any((got & 0x7F80) == 0x7F80), f"layer {l}: non-finite output (missing wait)"
+        assert np.array_equal(got, serial[l]), f"layer {l}: output differs from serial"
+        hk, hv = _want(b, synth.make_layer(b, l), poison, poison, src, dst, n_blocks)
+        assert np.array_equal(u16(outs[l].k), hk), f"layer {l}: offloaded K"
+        assert np.array_equal(u16(outs[l].v), hv), f"layer {l}: offloaded V"
+    assert np.all(t["offload_ms"] > 0) and np.all(t["load_ms"] > 0) and t["total_ms"] >= t["compute_end_ms"] > 0
+
+
 def test_staged_load_bitexact():
     b = synth.ragged_batch("ld", Hq=16, Hkv=4, d=128, prefix_lens=[512, 48, 0, 300], suffix_lens=[10, 20, 30, 1],
                            pool_blocks=100, seed=23)
