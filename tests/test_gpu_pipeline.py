@@ -140,6 +140,35 @@ def test_staged_pipeline_twice_on_one_workspace():
         assert np.array_equal(u16(L.out), serial[l]), f"layer {l}"
 
 
+def test_staged_pipeline_without_cached_blocks_and_one_layer():
+    """No cached prefix (nothing to load): the staged form needs no workspace and still
+    runs every layer's append and attention; and a one-layer staged pipeline."""
+    for p_len, n, need_ws in ((0, 3, False), (300, 1, True)):
+        b = synth.uniform_batch("pipe_edge", B=2, Hq=8, Hkv=2, d=64, p=p_len, s=77, pool_blocks=64, seed=7,
+                                num_layers=n, layer_seed_base=7000)
+        layers, poison = _layers(b, n)
+        serial = []
+        for L in layers:
+            L.run_serial("kernel_pull")
+            serial.append(u16(L.out).copy())
+            L.pool.k.copy_(torch.from_numpy(poison.view(np.int16)))
+            L.pool.v.copy_(torch.from_numpy(poison.view(np.int16)))
+            L.out.zero_()
+        torch.cuda.synchronize()
+        bp = layers[0].batch_plan()
+        assert (len(bp.src_blocks) > 0) == need_ws
+        ws = None
+        if need_ws:
+            ws = torch.empty(pcr.pipeline_staged_slot_bytes(len(bp.src_blocks), b.num_kv_heads, b.head_dim),
+                             dtype=torch.uint8, device="cuda")
+        copy_s, scat_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+        say(f"[gpu] staged pipeline, prefix {p_len}, {n} layer(s)")
+        pcr.pipeline_run_staged([L.layer_io() for L in layers], bp, ws, copy_s, scat_s, comp_s)
+        torch.cuda.synchronize()
+        for l, L in enumerate(layers):
+            assert np.array_equal(u16(L.out), serial[l]), f"prefix {p_len} layer {l}"
+
+
 def test_pipeline_partial_prefix_block_ordering():
     """p % 16 != 0: the last cached block is loaded whole and then partly
     overwritten by the append; the pipeline must keep that order per layer."""
