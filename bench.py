@@ -994,6 +994,11 @@ def _main(args, sampler):
     if args.pipeline_only:
         pb = workload(args.pipeline_workload)
         pst = measure_step(pb, args.steps, args.warmup)
+        pcr.prefill_attn_set_schedule("key_halves")   # the pull-load pipeline's attention schedule
+        try:
+            pst_keys = measure_step(pb, args.steps, args.warmup)
+        finally:
+            pcr.prefill_attn_set_schedule("auto")
         pld = measure_load(pb)
         dist = pb.num_layers if pb.name == "l8b_pipe32" else 6
         lbp = _setup_pipeline(pb, dist)
@@ -1005,9 +1010,10 @@ def _main(args, sampler):
                                                                                             sg["scatter_ms"]),
                                           reps=args.pipeline_reps, distinct=dist, layers_bp=lbp)
             else:
-                res[m] = measure_pipeline(pb, m, pld[m]["ms"], pst["step_ms"], reps=args.pipeline_reps, distinct=dist,
-                                          layers_bp=lbp)
-        print(json.dumps({"pipeline": res, "load": pld, "step_ms": pst["step_ms"]}), flush=True)
+                res[m] = measure_pipeline(pb, m, pld[m]["ms"], pst_keys["step_ms"], reps=args.pipeline_reps,
+                                          distinct=dist, layers_bp=lbp)
+        print(json.dumps({"pipeline": res, "load": pld, "step_ms": pst["step_ms"],
+                          "step_ms_key_halves": pst_keys["step_ms"]}), flush=True)
         return 0
 
     batch = workload(args.workload)
@@ -1046,21 +1052,31 @@ def _main(args, sampler):
             distinct = pb.num_layers if pb.name == "l8b_pipe32" else 6
             _say(f"[bench] pipeline: {pb.name} ({pb.num_layers} layers, {distinct} distinct layer data sets)")
             pst = pst or measure_step(pb, 20, 3, min_warm_ms=200.0)
+            # the pipelines with pull loads run their attention with key halves (the
+            # default schedule may take row halves for this size): their isolated step
+            # is measured that way too
+            pcr.prefill_attn_set_schedule("key_halves")
+            try:
+                pst_keys = measure_step(pb, 20, 3, min_warm_ms=200.0)
+            finally:
+                pcr.prefill_attn_set_schedule("auto")
             pld = pld or measure_load(pb, reps=4)
             lbp = _setup_pipeline(pb, distinct)
             recs = {}
             for m in pipeline_methods:
                 if m == "staged":
                     sg = pld["dma_staged"]
-                    rec = measure_pipeline(pb, "staged", sg["ms"], pst["step_ms"], reps=2, distinct=distinct,
+                    step = pst
+                    rec = measure_pipeline(pb, "staged", sg["ms"], step["step_ms"], reps=2, distinct=distinct,
                                            staged_stages=(sg["transfer_ms"], sg["scatter_ms"]), layers_bp=lbp)
                     rec["load_GBps"] = sg["GBps"]
                 else:
-                    rec = measure_pipeline(pb, m, pld[method]["ms"], pst["step_ms"], reps=2, distinct=distinct,
+                    step = pst_keys
+                    rec = measure_pipeline(pb, m, pld[method]["ms"], step["step_ms"], reps=2, distinct=distinct,
                                            layers_bp=lbp)
                     rec["load_GBps"] = pld[method]["GBps"]
                 rec["attn_tflops"] = attention_flops(pb.prefix_lens, pb.suffix_lens, pb.num_q_heads,
-                                                     pb.head_dim) / (pst["attn_b2b_ms"] * 1e-3) / 1e12
+                                                     pb.head_dim) / (step["attn_b2b_ms"] * 1e-3) / 1e12
                 recs[m] = rec
             del lbp
             torch.cuda.synchronize()
@@ -1082,7 +1098,7 @@ def _main(args, sampler):
                 for om, key in (("dma_staged", "dma_staged"), ("kernel_pull", "kernel_push")):
                     _say(f"[bench] pipeline with offload ({key}): {pb.name}")
                     pipelines[f"{pb.name}_offload_{key}"] = measure_pipeline_offload(
-                        pb, method, pld[method]["ms"], pst["step_ms"], off[key]["ms"], osrc, odst,
+                        pb, method, pld[method]["ms"], pst_keys["step_ms"], off[key]["ms"], osrc, odst,
                         offload_method=om, distinct=6)
                 _say(f"[bench] pipeline with staged loads and offload (dma_staged): {pb.name}")
                 sg = pld["dma_staged"]

@@ -244,6 +244,29 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
                                    void *stream);
 
 /*
+ * pcr_prefill_attn_set_schedule -- how pcr_prefix_prefill_attn (and the pipelines'
+ * attention) divides a launch among workgroups; a tuning and testing control, not
+ * part of the method. Every schedule computes the same result (Sec. 2.2).
+ *   PCR_ATTN_SCHEDULE_AUTO (the default): row halves when that still gives at
+ *     least two workgroups per compute unit, else key halves; pcr_pipeline_run and
+ *     pcr_pipeline_run_offload, whose pull-kernel loads share the compute units
+ *     with the attention, take key halves (shorter workgroups let the copy
+ *     workgroups onto a compute unit sooner);
+ *   PCR_ATTN_SCHEDULE_KEY_HALVES: 128 packed query rows per workgroup, the two
+ *     wave groups on the two halves of the key range, merged at the end;
+ *   PCR_ATTN_SCHEDULE_ROW_HALVES: 256 packed query rows per workgroup, each wave
+ *     group on 128 of them over the whole key range (half the workgroups, each
+ *     with one start-up and no merge for twice the work).
+ * Batches of more than 128 sequences use key halves whatever the setting.
+ * Process-wide; takes effect at the next launch. PCR_ERR_INVALID_ARG for an
+ * unknown value.
+ */
+#define PCR_ATTN_SCHEDULE_AUTO 0
+#define PCR_ATTN_SCHEDULE_KEY_HALVES 1
+#define PCR_ATTN_SCHEDULE_ROW_HALVES 2
+pcr_status pcr_prefill_attn_set_schedule(int32_t schedule);
+
+/*
  * pcr_decode_attn -- one decode step: attention of one new query token per
  * sequence over every key of that sequence (Sec. 2.2 with a one-token suffix:
  * the output equals the last row of a full prefill of the sequence).

@@ -7,11 +7,16 @@
 //
 // Work decomposition. The s*G query rows of one (sequence, kv head) pair,
 // G = Hq/Hkv, are packed token-major (row r = token r/G, head-in-group r%G)
-// so that all rows of a workgroup share one K/V stream. A workgroup of 8 waves
-// takes 128 packed rows. Waves 0-3 and 4-7 form two groups that hold the same
-// rows (32 per wave) and walk the two halves of the key range, so each SIMD
-// runs one wave of each group: one wave's softmax overlaps the other's
-// matrix work. The halves are merged through LDS at the end.
+// so that all rows of a workgroup share one K/V stream. A workgroup has 8 waves in
+// two groups (waves 0-3 and 4-7, 32 rows per wave), so each SIMD runs one wave of
+// each group: one wave's softmax overlaps the other's matrix work. Two schedules:
+//   key halves: the workgroup takes 128 packed rows; both groups hold the same rows
+//     and walk the two halves of the key range, merged through LDS at the end;
+//   row halves: the workgroup takes 256 packed rows, 128 per group, and both groups
+//     walk the whole key range, group 1 one phase behind; no merge.
+// Row halves give each workgroup twice the work for one start-up and no merge; the
+// host takes them when the launch still has at least two workgroups per compute
+// unit, key halves otherwise (twice the workgroups for small launches).
 //
 // Per wave and 64-key tile (4 pool blocks), with v_mfma_f32_32x32x16_bf16:
 //   S^T[key][q] = K Q^T   A = K rows from LDS, B = this wave's Q (registers)
@@ -40,6 +45,7 @@
 // hit distinct banks; the swizzle is applied through the source address of
 // each lane, since a direct load writes lane l's 16 bytes at base + 16*l.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "pcr_internal.h"
@@ -59,7 +65,7 @@ typedef unsigned short u16;
 
 constexpr int kGroupWaves = 4;
 constexpr int kRowsPerWave = 32;
-constexpr int kRowsPerWG = kGroupWaves * kRowsPerWave;   // 128 rows, shared by both groups
+constexpr int kRowsPerWG = kGroupWaves * kRowsPerWave;   // 128 rows (key halves: both groups)
 constexpr int kThreads = 2 * kGroupWaves * 64;           // 512
 constexpr int kTileKeys = 64;
 constexpr int kTileBlocks = kTileKeys / kBlockSize;
@@ -163,7 +169,7 @@ struct AttnWorkMap {
     int32_t count[kMaxMapSeqs];         // the slot's new tokens s
 };
 
-template <int D>
+template <int D, bool ROWS>
 __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
@@ -179,6 +185,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     constexpr int kSlabs = (int)(kPayloadBytes / 1024);       // 1 KB slabs per payload
     static_assert(kGroupWaves % kSlabs == 0, "slab-to-wave mapping");
     constexpr int kKLoads = Geo::KLOADS, kVLoads = Geo::VLOADS;
+    constexpr int RPW = ROWS ? 2 * kRowsPerWG : kRowsPerWG;   // packed rows per workgroup
 
     // Per group: K buffers 0/1 then V buffers 0/1 (double-buffered, tile j in buffer j&1);
     // the whole array is reused for the merge at the end.
@@ -240,18 +247,19 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         }
     }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int grp = wave >> 2;              // 0: first half of the keys, 1: second half
+    const int grp = wave >> 2;              // key halves: which half of the keys; row halves: of the rows
     const int wg = wave & 3;                // wave within the group (selects the rows)
     const int qc = lane & 31, half = lane >> 5;
 
     const int G = Hq / Hkv;
     const int rows_total = s * G;
-    const int row0 = rt * kRowsPerWG;
+    const int row0 = rt * RPW;
     if (s <= 0 || row0 >= rows_total || T <= 0) return;   // uniform over the workgroup
     const int total = p + s;
 
     // This lane's packed query row (rows past the end compute a copy of the last row).
-    const int R = row0 + wg * kRowsPerWave + qc;
+    const int wrow0 = row0 + (ROWS ? grp * kRowsPerWG : 0) + wg * kRowsPerWave;   // this wave's first row
+    const int R = wrow0 + qc;
     const bool row_valid = R < rows_total;
     const int Rc = row_valid ? R : rows_total - 1;
     const int i = Rc / G, hl = Rc - i * G;
@@ -259,12 +267,14 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int limit = p + i;                         // last key this row attends to
     const int64_t tq = (int64_t)t0 + i;
 
-    const int wg_last = min(rows_total - 1, row0 + kRowsPerWG - 1);
+    const int wg_last = min(rows_total - 1, row0 + RPW - 1);
     const int ntiles = (p + wg_last / G) / kTileKeys + 1;
-    const int split = (ntiles + 1) >> 1;             // group 0: [0, split), group 1: [split, ntiles)
-    const int tile_begin = grp ? split : 0;
-    const int n = (grp ? ntiles : split) - tile_begin;   // this group's tiles
-    const int w_first = min(rows_total - 1, row0 + wg * kRowsPerWave);
+    // key halves: group 0 takes tiles [0, split), group 1 [split, ntiles); row halves:
+    // both take every tile
+    const int split = ROWS ? ntiles : (ntiles + 1) >> 1;
+    const int tile_begin = (!ROWS && grp) ? split : 0;
+    const int n = (ROWS || !grp ? split : ntiles) - tile_begin;   // this group's tiles
+    const int w_first = min(rows_total - 1, wrow0);
     const int w_min_limit = p + w_first / G;
     const int valid_blocks = min((total + kBlockSize - 1) / kBlockSize, max_blocks);
 
@@ -571,6 +581,9 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // C(j+1) reads them. Rows whose causal limit ends before a tile get P = 0 there.
     // Block offsets travel one phase ahead: at C(j), ids_v holds tile j+1's (for
     // V(j+1)) and ids_k tile j+2's (for K(j+2)).
+    // With row halves both groups walk every tile, each through its own buffers
+    // (sharing one copy would need a branch around every load of group 1's clusters,
+    // and loads are not what bounds a phase).
     int64_t ids_v[kTileBlocks], ids_k[kTileBlocks];   // payload byte offsets
     tile_ids(0, ids_raw);
     to_offs(ids_raw, ids_v);
@@ -584,7 +597,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     wait_vmem();
     __syncthreads();
 
-    const int n0 = split, n1 = ntiles - split;
+    const int n0 = split, n1 = ROWS ? ntiles : ntiles - split;
     const int phases = max(2 * n0 + 1, 2 * n1 + 2);
     int ph = 0;
     auto phase_end = [&]() {
@@ -653,7 +666,27 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     }
     while (ph < phases) phase_end();
 
-    // ---- merge the two key halves through LDS, normalise, store ----
+    if constexpr (ROWS) {
+        // ---- row halves: every group saw all keys of its rows; normalise, store ----
+        const float inv = 1.f / (l_run + ((lane & 16) ? tsum[1] : tsum[0]));
+        if (row_valid && tq < T) {
+            u16 *orow = out + (tq * Hq + h) * D;
+#pragma unroll
+            for (int k = 0; k < MT; ++k)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    f32x4 v;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) v[c] = o_acc[k][4 * r4 + c] * inv;
+                    const bf16x4 bv = __builtin_convertvector(v, bf16x4);
+                    const int d0 = 32 * k + 8 * r4 + 4 * half;
+                    *reinterpret_cast<u32x2 *>(orow + d0) = __builtin_bit_cast(u32x2, bv);
+                }
+        }
+        return;
+    }
+
+    // ---- key halves: merge the two halves through LDS, normalise, store ----
     // Each group finalises half of the head dims (group 0 the first MT/2 blocks of 32,
     // group 1 the rest): it sends the partner wave holding the same rows the other half
     // of its accumulator and its (m, l), then merges the half it received.
@@ -709,35 +742,81 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 
 int attn_rows_per_workgroup(int) { return kRowsPerWG; }
 
+namespace {
+// Schedule override (pcr_prefill_attn_set_schedule): 0 chooses per launch.
+std::atomic<int> g_schedule{PCR_ATTN_SCHEDULE_AUTO};
+// Compute units of each device, read once.
+std::atomic<int> g_cu_count[64];
+
+int device_cus()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int cu = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (cu <= 0) {
+        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
+        g_cu_count[dev].store(cu, std::memory_order_relaxed);
+    }
+    return cu;
+}
+
+template <int D, bool ROWS>
+void launch_attn(dim3 grid, hipStream_t s, const u16 *qq, const u16 *pk, const u16 *pv, const pcr_kv_pool &pool,
+                 const int32_t *block_tables, int32_t max_blocks, const int32_t *prefix_lens,
+                 const int32_t *cu_suffix, int32_t num_q_heads, int32_t T, int32_t B, int32_t row_tiles,
+                 float scale_log2, float rescale_thr, u16 *oo, const AttnWorkMap &wm)
+{
+    hipLaunchKernelGGL((prefill_attn_kernel<D, ROWS>), grid, dim3(kThreads), 0, s, qq, pk, pv, pool.num_blocks,
+                       pool.num_kv_heads, block_tables, max_blocks, prefix_lens, cu_suffix, num_q_heads, T, B,
+                       row_tiles, scale_log2, rescale_thr, oo, wm);
+}
+}  // namespace
+
+void attn_set_schedule(int schedule) { g_schedule.store(schedule, std::memory_order_relaxed); }
+
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *block_tables, int32_t max_blocks,
                                       const int32_t *prefix_lens, const int32_t *cu_suffix,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
-                                      hipStream_t s)
+                                      hipStream_t s, int auto_schedule)
 {
     const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv;
     AttnWorkMap wm;
     wm.n_seq = 0;
     wm.per_head = 0;
     int64_t n_items;
+    bool rows = false;
     if (B <= kMaxMapSeqs) {
-        int32_t tiles[kMaxMapSeqs], keys[kMaxMapSeqs];
+        int32_t keys[kMaxMapSeqs];
+        int64_t rows_of[kMaxMapSeqs];
         int n = 0;
+        int64_t tiles_rows = 0;   // row tiles of 256 rows over all sequences, one kv head
         for (int b = 0; b < B; ++b) {
             const int64_t sb = (int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b];
             if (sb <= 0) continue;
             wm.seq[n] = b;
-            tiles[b] = (int32_t)((sb * G + kRowsPerWG - 1) / kRowsPerWG);
+            rows_of[b] = sb * G;
             keys[b] = (int32_t)(host_prefix_lens[b] + sb);
+            tiles_rows += (rows_of[b] + 2 * kRowsPerWG - 1) / (2 * kRowsPerWG);
             ++n;
         }
+        if (n == 0) return hipSuccess;
+        // Row halves when the launch keeps at least two workgroups per compute unit
+        // with them (each workgroup then pays its start-up and end for twice the work),
+        // unless the caller prefers key halves (shorter workgroups free a compute unit
+        // sooner for copy kernels that share the device).
+        int sched = g_schedule.load(std::memory_order_relaxed);
+        if (sched == PCR_ATTN_SCHEDULE_AUTO) sched = auto_schedule;
+        rows = sched == PCR_ATTN_SCHEDULE_ROW_HALVES ||
+               (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)device_cus());
+        const int64_t rpw = rows ? 2 * kRowsPerWG : kRowsPerWG;
         std::stable_sort(wm.seq, wm.seq + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
         int32_t cum = 0;
         for (int k = 0; k < n; ++k) {
             const int b = wm.seq[k];
-            cum += tiles[b];
+            cum += (int32_t)((rows_of[b] + rpw - 1) / rpw);
             wm.tiles_end[k] = cum;
             wm.prefix[k] = host_prefix_lens[b];
             wm.first[k] = host_cu_suffix[b];
@@ -745,7 +824,6 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
         }
         wm.n_seq = n;
         wm.per_head = cum;
-        if (n == 0) return hipSuccess;
         n_items = (Hkv % kXcds == 0) ? (int64_t)wm.per_head * Hkv
                                      : ((int64_t)wm.per_head * Hkv + kXcds - 1) / kXcds * kXcds;
     } else {
@@ -758,14 +836,21 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
     auto *pk = static_cast<const u16 *>(pool.k);
     auto *pv = static_cast<const u16 *>(pool.v);
     auto *oo = static_cast<u16 *>(out);
-    if (pool.head_dim == 128)
-        hipLaunchKernelGGL(prefill_attn_kernel<128>, grid, dim3(kThreads), 0, s, qq, pk, pv,
-                           pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
-    else
-        hipLaunchKernelGGL(prefill_attn_kernel<64>, grid, dim3(kThreads), 0, s, qq, pk, pv,
-                           pool.num_blocks, pool.num_kv_heads, block_tables, max_blocks, prefix_lens,
-                           cu_suffix, num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+    if (pool.head_dim == 128) {
+        if (rows)
+            launch_attn<128, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                   num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+        else
+            launch_attn<128, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                    num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+    } else {
+        if (rows)
+            launch_attn<64, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                  num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+        else
+            launch_attn<64, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                   num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+    }
     return hipGetLastError();
 }
 

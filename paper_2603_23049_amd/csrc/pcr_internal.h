@@ -47,7 +47,7 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
-                                      hipStream_t s);
+                                      hipStream_t s, int auto_schedule);
 
 // Decode attention (decode.hip). The key range of each (sequence, kv head) is cut
 // into n_split chunks of `chunk` keys; bound_split is the split count for the
@@ -92,8 +92,19 @@ pcr_status offload_with(const pcr_kv_pool *src, const int32_t *src_blocks, const
                         const int32_t *dst_blocks, int32_t n, pcr_load_method method, void *workspace,
                         int64_t workspace_bytes, void *stream);
 
-// Rows of packed (token, head-in-group) queries one attention workgroup handles.
+// pcr_prefix_prefill_attn with a schedule preference: when the process-wide schedule
+// is PCR_ATTN_SCHEDULE_AUTO, auto_schedule PCR_ATTN_SCHEDULE_KEY_HALVES takes key
+// halves whatever the size (PCR_ATTN_SCHEDULE_AUTO: the size rule).
+pcr_status prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                               int32_t max_blocks, const int32_t *prefix_lens, const int32_t *cu_suffix,
+                               const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
+                               int32_t num_q_heads, float sm_scale, void *out, void *stream, int auto_schedule);
+
+// Rows of packed (token, head-in-group) queries one attention workgroup handles with
+// key halves (the most row tiles any schedule launches per sequence).
 int attn_rows_per_workgroup(int head_dim);
+// Process-wide attention schedule (PCR_ATTN_SCHEDULE_*), read at each launch.
+void attn_set_schedule(int schedule);
 
 // Every argument check of pcr_prefix_prefill_attn, with no launch (errors name `who`);
 // on success *T_out is the suffix token count (0: nothing to do) and *max_tiles_out

@@ -209,10 +209,13 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
         st = pcr_append_kv(&layers[l].pool, layers[l].k_new, layers[l].v_new, batch->slot_mapping,
                                       batch->T, compute_stream);
         if (st) return st;
-        st = pcr_prefix_prefill_attn(layers[l].q, &layers[l].pool, batch->block_tables, batch->max_blocks,
-                                     batch->prefix_lens, batch->cu_suffix, batch->host_prefix_lens,
-                                     batch->host_cu_suffix, batch->B, batch->num_q_heads, batch->sm_scale,
-                                     layers[l].out, compute_stream);
+        // Beside pull-kernel loads the attention takes key halves: its shorter workgroups
+        // let a load's copy workgroups onto a compute unit sooner.
+        st = prefix_prefill_attn(layers[l].q, &layers[l].pool, batch->block_tables, batch->max_blocks,
+                                 batch->prefix_lens, batch->cu_suffix, batch->host_prefix_lens,
+                                 batch->host_cu_suffix, batch->B, batch->num_q_heads, batch->sm_scale,
+                                 layers[l].out, compute_stream,
+                                 staged ? PCR_ATTN_SCHEDULE_AUTO : PCR_ATTN_SCHEDULE_KEY_HALVES);
         if (st) return st;
         PCR_HIP(hipEventRecord(ev_cend(l), ks), "pcr_pipeline_run: record compute end");
         if (with_offload) {

@@ -650,18 +650,8 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const
                                    const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
                                    int32_t num_q_heads, float sm_scale, void *out, void *stream)
 {
-    g_err[0] = 0;
-    int64_t T = 0, max_tiles = 0;
-    pcr_status st = attn_check(q, pool, block_tables, max_blocks, prefix_lens, cu_suffix, host_prefix_lens,
-                               host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T,
-                               &max_tiles);
-    if (st || T == 0) return st;
-    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                              host_prefix_lens, host_cu_suffix, B,
-                                              num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,
-                                              static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "pcr_prefix_prefill_attn: launch");
-    return PCR_OK;
+    return pcr::prefix_prefill_attn(q, pool, block_tables, max_blocks, prefix_lens, cu_suffix, host_prefix_lens,
+                                    host_cu_suffix, B, num_q_heads, sm_scale, out, stream, PCR_ATTN_SCHEDULE_AUTO);
 }
 
 static pcr_status decode_heads_ok(int32_t num_q_heads, int32_t num_kv_heads, const char *who)
@@ -683,6 +673,16 @@ static pcr_status device_cu_count(int32_t *n_cu, const char *who)
     e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_fail(e, who);
     *n_cu = cu > 0 ? cu : 1;
+    return PCR_OK;
+}
+
+pcr_status pcr_prefill_attn_set_schedule(int32_t schedule)
+{
+    g_err[0] = 0;
+    if (schedule != PCR_ATTN_SCHEDULE_AUTO && schedule != PCR_ATTN_SCHEDULE_KEY_HALVES &&
+        schedule != PCR_ATTN_SCHEDULE_ROW_HALVES)
+        return fail(PCR_ERR_INVALID_ARG, "pcr_prefill_attn_set_schedule: unknown schedule %d", (int)schedule);
+    attn_set_schedule(schedule);
     return PCR_OK;
 }
 
@@ -823,6 +823,25 @@ pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, i
 }  // extern "C"
 
 namespace pcr {
+
+pcr_status prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
+                               int32_t max_blocks, const int32_t *prefix_lens, const int32_t *cu_suffix,
+                               const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
+                               int32_t num_q_heads, float sm_scale, void *out, void *stream, int auto_schedule)
+{
+    g_err[0] = 0;
+    int64_t T = 0, max_tiles = 0;
+    pcr_status st = attn_check(q, pool, block_tables, max_blocks, prefix_lens, cu_suffix, host_prefix_lens,
+                               host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T,
+                               &max_tiles);
+    if (st || T == 0) return st;
+    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
+                                              host_prefix_lens, host_cu_suffix, B,
+                                              num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,
+                                              static_cast<hipStream_t>(stream), auto_schedule);
+    if (e != hipSuccess) return hip_fail(e, "pcr_prefix_prefill_attn: launch");
+    return PCR_OK;
+}
 
 pcr_status load_staged_split(const pcr_host_kv *src, const int32_t *src_blocks, const pcr_kv_pool *dst,
                              const int32_t *dst_blocks, int32_t n, void *workspace, int64_t workspace_bytes,

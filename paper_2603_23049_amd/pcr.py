@@ -35,7 +35,7 @@ LOAD_METHODS = {"auto": LOAD_AUTO, "dma_batch": LOAD_DMA_BATCH, "dma_per_block":
 EXPORTS = ["pcr_plan", "pcr_plan_offload", "pcr_load_kv_layer", "pcr_load_kv_layer_method",
            "pcr_offload_kv_layer", "pcr_offload_kv_layer_method", "pcr_offload_kv_layer_staged",
            "pcr_load_kv_layer_staged", "pcr_append_kv",
-           "pcr_prefix_prefill_attn", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_staged",
+           "pcr_prefix_prefill_attn", "pcr_prefill_attn_set_schedule", "pcr_decode_attn", "pcr_decode_attn_noalloc", "pcr_decode_attn_workspace_size", "pcr_gather_kv", "pcr_pipeline_run", "pcr_pipeline_run_staged",
            "pcr_pipeline_run_offload", "pcr_pipeline_run_offload_staged",
            "pcr_store_open", "pcr_store_write_async", "pcr_store_read_async", "pcr_store_wait",
            "pcr_store_poll", "pcr_store_stats", "pcr_store_close", "pcr_last_error", "pcr_version"]
@@ -90,6 +90,7 @@ def lib():
         L.pcr_append_kv.argtypes = [ctypes.POINTER(_Pool), P, P, P, i32, P]
         L.pcr_prefix_prefill_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, P, P, i32, i32,
                                               ctypes.c_float, P, P]
+        L.pcr_prefill_attn_set_schedule.argtypes = [i32]
         L.pcr_decode_attn.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, ctypes.c_float, P, P,
                                       i64, P]
         L.pcr_decode_attn_noalloc.argtypes = [P, ctypes.POINTER(_Pool), P, i32, P, P, i32, i32, ctypes.c_float, P,
@@ -313,6 +314,15 @@ def decode_attn_workspace_bytes(B: int, num_q_heads: int, num_kv_heads: int, hea
     _check(lib().pcr_decode_attn_workspace_size(int(B), int(num_q_heads), int(num_kv_heads), int(head_dim),
                                                 int(max_context), ctypes.byref(n)))
     return int(n.value)
+
+
+ATTN_SCHEDULES = {"auto": 0, "key_halves": 1, "row_halves": 2}
+
+
+def prefill_attn_set_schedule(schedule: str = "auto"):
+    """pcr_prefill_attn_set_schedule: process-wide attention schedule ("auto",
+    "key_halves" or "row_halves")."""
+    _check(lib().pcr_prefill_attn_set_schedule(ATTN_SCHEDULES[schedule]))
 
 
 def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, num_q_heads: int, out,

@@ -1,5 +1,6 @@
 """GPU-side test plumbing: numpy bf16 bit arrays <-> torch tensors, and one
 layer of a batch set up for the HIP path through the C ABI binding."""
+import contextlib
 import sys
 
 import numpy as np
@@ -11,6 +12,18 @@ from paper_2603_23049_amd import pcr, synth
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+@contextlib.contextmanager
+def attn_schedule(name: str):
+    """Runs the block under one attention schedule, then restores the default ("auto").
+    The pipelines with pull-kernel loads take key halves under "auto", so their serial
+    references are computed with key halves."""
+    pcr.prefill_attn_set_schedule(name)
+    try:
+        yield
+    finally:
+        pcr.prefill_attn_set_schedule("auto")
 
 
 def dev(a: np.ndarray) -> torch.Tensor:

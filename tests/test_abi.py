@@ -178,6 +178,11 @@ def test_argument_validation_before_any_device_work():
     bat2.num_q_heads = 3
     assert L.pcr_pipeline_run_offload(lay2, None, 2, P(bat2), None, None, 0, 0, 0, None, 0, 0x5, 0x6, 0x7,
                                       None) == pcr.PCR_ERR_UNSUPPORTED
+    # attention schedule: three values, anything else refused
+    assert L.pcr_prefill_attn_set_schedule(3) == pcr.PCR_ERR_INVALID_ARG
+    assert L.pcr_prefill_attn_set_schedule(-1) == pcr.PCR_ERR_INVALID_ARG
+    for sch in (2, 1, 0):
+        assert L.pcr_prefill_attn_set_schedule(sch) == pcr.PCR_OK
     # staged pipeline: streams, workspace and pool shapes are checked before anything is queued
     slot = 2 * 3 * 16 * 2 * 64 * 2        # 3 pairs of (16-token, 2-head, d=64) K and V blocks
     bat2.n_pairs = 3

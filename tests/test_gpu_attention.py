@@ -3,6 +3,7 @@
 Tolerance (bf16 inputs, fp32 accumulation, bf16 output): max |err| <= 2e-2 and
 mean |err| <= 2e-3 against the fp64 oracle. Beyond the tolerance the HIP path
 must be deterministic and bit-invariant to which physical blocks hold the KV.
+Each test runs under both workgroup schedules (key halves, row halves).
 """
 import numpy as np
 import pytest
@@ -16,6 +17,16 @@ from gpuio import GpuLayer, MAX_ABS, MEAN_ABS, error_stats, say, u16
 pytestmark = pytest.mark.gpu
 
 BS = 16
+
+
+@pytest.fixture(autouse=True, params=["key_halves", "row_halves"])
+def schedule(request):
+    """Every test of this module runs under both attention schedules (the default picks
+    one per launch from its size; forcing each covers small and odd shapes with both)."""
+    from paper_2603_23049_amd import pcr
+    pcr.prefill_attn_set_schedule(request.param)
+    yield request.param
+    pcr.prefill_attn_set_schedule("auto")
 
 
 def _pools(b, seed=99):

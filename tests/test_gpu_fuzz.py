@@ -56,8 +56,15 @@ def test_random_shapes_prefill_and_decode(seed):
     pk0, pv0 = synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
     say(f"[gpu] fuzz seed={seed} G={G} Hkv={Hkv} d={d} B={b.B} T={b.T} prefix={pl} suffix={sl}")
 
-    L = GpuLayer(b, data, pk0, pv0)
-    L.run_serial("kernel_pull")
+    # even seeds under the key-halves attention schedule, odd seeds under row halves
+    sched = ("key_halves", "row_halves")[seed % 2]
+    say(f"    attention schedule {sched}")
+    pcr.prefill_attn_set_schedule(sched)
+    try:
+        L = GpuLayer(b, data, pk0, pv0)
+        L.run_serial("kernel_pull")
+    finally:
+        pcr.prefill_attn_set_schedule("auto")
     plan = odm.plan(b.prefix_lens, b.suffix_lens, b.block_tables, b.host_blocks, BS)
     pk, pv = odm.pool_after_layer(pk0, pv0, data.host_k, data.host_v, plan, data.k_new, data.v_new, BS)
     cu = plan[3]

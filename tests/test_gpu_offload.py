@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from paper_2603_23049_amd import pcr, synth
-from gpuio import GpuLayer, pinned, say, u16
+from gpuio import attn_schedule, GpuLayer, pinned, say, u16
 from oracle import datamove as odm
 
 pytestmark = pytest.mark.gpu
@@ -213,7 +213,8 @@ def test_pipeline_with_offload_full_size(method):
     base = [GpuLayer(b, synth.make_layer(b, l), poison, poison) for l in range(distinct)]
     serial = []
     for L in base:
-        L.run_serial("kernel_pull")
+        with attn_schedule("key_halves"):   # the pull-load pipeline's attention schedule
+            L.run_serial("kernel_pull")
         serial.append(L.out.clone())
         L.pool.k.fill_(int(NAN_BITS))
         L.pool.v.fill_(int(NAN_BITS))

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 from paper_2603_23049_amd import pcr, synth
-from gpuio import GpuLayer, MAX_ABS, MEAN_ABS, error_stats, pinned, say, u16
+from gpuio import GpuLayer, MAX_ABS, MEAN_ABS, attn_schedule, error_stats, pinned, say, u16
 from oracle import attention as oattn
 from oracle import datamove as odm
 
@@ -208,9 +208,12 @@ def _special_layers(n):
 
 def _full_pipeline(name):
     """Runs the named pipeline once per test session with method "auto", then again with
-    staged loads (every pool poisoned with NaN bit patterns before each run) and checks, for every layer, that its pool is the
+    staged loads (every pool poisoned with NaN bit patterns before each run; the
+    pull-load pipeline's attention takes key halves, the staged one's the default
+    schedule, row halves at the 70B and compute-bound shapes) and checks, for every layer, that its pool is the
     oracle's bit for bit and its output equals its data set's serialized result bit for
-    bit. Keeps, for the first, middle and last layers, the output and the oracle's inputs."""
+    bit. Keeps, for the first, middle and last layers, the staged run's output and the
+    oracle's inputs."""
     if name in _FULL_RESULTS:
         return _FULL_RESULTS[name]
     mk, distinct = FULL[name]
@@ -223,13 +226,17 @@ def _full_pipeline(name):
     say(f"[gpu] pipeline {b.name}: {n} layers, {n_sets} distinct data sets (generating)")
     datas = synth.make_layers(b, range(n_sets))
     base = [GpuLayer(b, datas[k], poison, poison) for k in range(n_sets)]
-    serial = []
+    # serial references: under key halves for the pull-load pipeline (which takes them),
+    # under the default schedule for the staged one
+    serial = {"auto": [], "staged": []}
     for L in base:
-        L.run_serial("auto")
-        serial.append(L.out.clone())
-        L.pool.k.fill_(int(NAN_BITS))
-        L.pool.v.fill_(int(NAN_BITS))
-        L.out.zero_()
+        for form, sched in (("auto", "key_halves"), ("staged", "auto")):
+            with attn_schedule(sched):
+                L.run_serial("auto")
+            serial[form].append(L.out.clone())
+            L.pool.k.fill_(int(NAN_BITS))
+            L.pool.v.fill_(int(NAN_BITS))
+            L.out.zero_()
     ios = [L.layer_io() for L in base]
     for l in range(n_sets, n):
         src = base[sets[l]]
@@ -272,8 +279,8 @@ def _full_pipeline(name):
                 io = ios[l]
                 assert torch.equal(io.pool.k, pk_d) and torch.equal(io.pool.v, pv_d), \
                     f"layer {l}: pool differs ({form})"
-                assert torch.equal(io.out, serial[k]), f"layer {l}: pipeline output differs from serial ({form})"
-                if l in special and form == "auto":
+                assert torch.equal(io.out, serial[form][k]), f"layer {l}: pipeline output differs from serial ({form})"
+                if l in special and form == "staged":
                     keep[l] = {"out": u16(io.out), "q": data.q, "pk": pk, "pv": pv}
             del pk_d, pv_d
         say(f"    every layer's pool equals the oracle's and every output the serial result, bit for bit")
