@@ -745,21 +745,6 @@ int attn_rows_per_workgroup(int) { return kRowsPerWG; }
 namespace {
 // Schedule override (pcr_prefill_attn_set_schedule): 0 chooses per launch.
 std::atomic<int> g_schedule{PCR_ATTN_SCHEDULE_AUTO};
-// Compute units of each device, read once.
-std::atomic<int> g_cu_count[64];
-
-int device_cus()
-{
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    int cu = g_cu_count[dev].load(std::memory_order_relaxed);
-    if (cu <= 0) {
-        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-        g_cu_count[dev].store(cu, std::memory_order_relaxed);
-    }
-    return cu;
-}
-
 template <int D, bool ROWS>
 void launch_attn(dim3 grid, hipStream_t s, const u16 *qq, const u16 *pk, const u16 *pv, const pcr_kv_pool &pool,
                  const int32_t *block_tables, int32_t max_blocks, const int32_t *prefix_lens,
@@ -780,7 +765,7 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
-                                      hipStream_t s, int auto_schedule)
+                                      hipStream_t s, int auto_schedule, int n_cu)
 {
     const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv;
     AttnWorkMap wm;
@@ -810,7 +795,7 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
         int sched = g_schedule.load(std::memory_order_relaxed);
         if (sched == PCR_ATTN_SCHEDULE_AUTO) sched = auto_schedule;
         rows = sched == PCR_ATTN_SCHEDULE_ROW_HALVES ||
-               (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)device_cus());
+               (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)n_cu);
         const int64_t rpw = rows ? 2 * kRowsPerWG : kRowsPerWG;
         std::stable_sort(wm.seq, wm.seq + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
         int32_t cum = 0;

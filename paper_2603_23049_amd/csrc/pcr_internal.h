@@ -47,7 +47,9 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
                                       int32_t B, int32_t num_q_heads, int32_t T,
                                       int32_t max_row_tiles, float sm_scale, void *out,
-                                      hipStream_t s, int auto_schedule);
+                                      hipStream_t s, int auto_schedule, int n_cu);
+// Compute units of the current device (queried once per device).
+pcr_status device_cu_count(int32_t *n_cu, const char *who);
 
 // Decode attention (decode.hip). The key range of each (sequence, kv head) is cut
 // into n_split chunks of `chunk` keys; bound_split is the split count for the

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <unordered_map>
 #include <unordered_set>
@@ -665,16 +666,6 @@ static pcr_status decode_heads_ok(int32_t num_q_heads, int32_t num_kv_heads, con
     return PCR_OK;
 }
 
-static pcr_status device_cu_count(int32_t *n_cu, const char *who)
-{
-    int dev = 0, cu = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return hip_fail(e, who);
-    e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return hip_fail(e, who);
-    *n_cu = cu > 0 ? cu : 1;
-    return PCR_OK;
-}
 
 pcr_status pcr_prefill_attn_set_schedule(int32_t schedule)
 {
@@ -824,6 +815,26 @@ pcr_status pcr_gather_kv(const pcr_kv_pool *pool, const int32_t *block_tables, i
 
 namespace pcr {
 
+namespace {
+std::atomic<int32_t> g_cu_count[64];   // per device id, 0 until queried
+}  // namespace
+
+pcr_status device_cu_count(int32_t *n_cu, const char *who)
+{
+    int dev = 0, cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    if (dev >= 0 && dev < 64 && (cu = g_cu_count[dev].load(std::memory_order_relaxed)) > 0) {
+        *n_cu = cu;
+        return PCR_OK;
+    }
+    e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    *n_cu = cu > 0 ? cu : 1;
+    if (dev >= 0 && dev < 64) g_cu_count[dev].store(*n_cu, std::memory_order_relaxed);
+    return PCR_OK;
+}
+
 pcr_status prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
                                int32_t max_blocks, const int32_t *prefix_lens, const int32_t *cu_suffix,
                                const int32_t *host_prefix_lens, const int32_t *host_cu_suffix, int32_t B,
@@ -835,10 +846,13 @@ pcr_status prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int
                                host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T,
                                &max_tiles);
     if (st || T == 0) return st;
+    int32_t n_cu = 0;
+    st = device_cu_count(&n_cu, "pcr_prefix_prefill_attn");
+    if (st) return st;
     hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
                                               host_prefix_lens, host_cu_suffix, B,
                                               num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,
-                                              static_cast<hipStream_t>(stream), auto_schedule);
+                                              static_cast<hipStream_t>(stream), auto_schedule, n_cu);
     if (e != hipSuccess) return hip_fail(e, "pcr_prefix_prefill_attn: launch");
     return PCR_OK;
 }
