@@ -13,7 +13,8 @@
 //   key halves: the workgroup takes 128 packed rows; both groups hold the same rows
 //     and walk the two halves of the key range, merged through LDS at the end;
 //   row halves: the workgroup takes 256 packed rows, 128 per group, and both groups
-//     walk the whole key range, group 1 one phase behind; no merge.
+//     walk the whole key range, group 1 one phase behind, through one copy of each
+//     tile that group 0 loads; no merge.
 // Row halves give each workgroup twice the work for one start-up and no merge; the
 // host takes them when the launch still has at least two workgroups per compute
 // unit, key halves otherwise (twice the workgroups for small launches).
@@ -188,7 +189,8 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     constexpr int RPW = ROWS ? 2 * kRowsPerWG : kRowsPerWG;   // packed rows per workgroup
 
     // Per group: K buffers 0/1 then V buffers 0/1 (double-buffered, tile j in buffer j&1);
-    // the whole array is reused for the merge at the end.
+    // with row halves both groups use group 0's. The whole array is reused for the merge
+    // at the end of key halves.
     __shared__ __attribute__((aligned(1024))) char lds[2][2 * (Geo::KBYTES + Geo::VBYTES)];
 
     // XCD-aware order: workgroup L runs on XCD L % 8. The row tiles of one (sequence,
@@ -328,10 +330,11 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     for (int r = 0; r < 16; ++r) nbias[r] = 0.f;
 
     const int32_t *bt = block_tables + (int64_t)b * max_blocks;
-    auto kbuf = [&](int j) { return &lds[grp][(j & 1) * Geo::KBYTES]; };
-    auto vbuf = [&](int j) { return &lds[grp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
+    const int lgrp = ROWS ? 0 : grp;        // whose tile buffers this group reads
+    auto kbuf = [&](int j) { return &lds[lgrp][(j & 1) * Geo::KBYTES]; };
+    auto vbuf = [&](int j) { return &lds[lgrp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
     // The same buffers as LDS byte addresses, for the direct loads (no generic-pointer casts).
-    const uint32_t lds_addr = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)&lds[grp][0];
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)&lds[lgrp][0];
     auto kbuf_off = [&](int j) { return (uint32_t)((j & 1) * Geo::KBYTES); };
     auto vbuf_off = [&](int j) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
 
@@ -427,11 +430,12 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // V(j+1) and K(j+2), one per few MFMAs, so the texture path never backs up a wave.
     auto matrix_cluster = [&](auto pv_tag, auto qk_tag, int j, const bf16x8 (&pf)[kTileBlocks],
                               f32x16 (&st)[2], int64_t (&idv)[kTileBlocks], int64_t (&idk)[kTileBlocks],
-                              auto convert_tag) {
+                              auto convert_tag, auto load_tag) {
         constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
+        constexpr bool LOADS = decltype(load_tag)::value;
 
         constexpr int NPV = DO_PV ? kTileBlocks * MT : 0, NQK = DO_QK ? 2 * KSTEPS : 0, NALL = NPV + NQK;
-        constexpr int NLD = DO_QK ? kVLoads + kKLoads : 0;
+        constexpr int NLD = DO_QK && LOADS ? kVLoads + kKLoads : 0;
         constexpr int NLD1 = NLD > 0 ? NLD : 1;
         constexpr int EVERY = NALL / NLD1 > 0 ? NALL / NLD1 : 1;
         constexpr int kAhead = KAHEAD;
@@ -457,7 +461,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 #pragma unroll
         for (int i = 0; i < kAhead && i < NALL; ++i) fr[i] = frag(i);
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (decltype(convert_tag)::value) {
+        if constexpr (decltype(convert_tag)::value && LOADS) {
             // Block ids read in the preceding vector cluster (and waited for at its end)
             // become payload offsets here, while the first fragment reads are in flight.
 #pragma unroll
@@ -581,13 +585,18 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // C(j+1) reads them. Rows whose causal limit ends before a tile get P = 0 there.
     // Block offsets travel one phase ahead: at C(j), ids_v holds tile j+1's (for
     // V(j+1)) and ids_k tile j+2's (for K(j+2)).
-    // With row halves both groups walk every tile, each through its own buffers
-    // (sharing one copy would need a branch around every load of group 1's clusters,
-    // and loads are not what bounds a phase).
+    // With row halves both groups walk the same tiles, and only group 0 loads them:
+    // group 1 reads group 0's buffers one phase later. Two buffers per operand still
+    // suffice: group 0's C(j) (phase 2j+2 counted from the first barrier) overwrites the
+    // buffers of V(j-1) and K(j), whose last reader is group 1's C(j-1) in phase 2j+1,
+    // and the barrier between phases orders the two. The LDS then takes one tile's
+    // direct-load writes per two phases instead of two, on a path whose fragment reads
+    // already run near its bandwidth.
+    const bool loader = !ROWS || grp == 0;
     int64_t ids_v[kTileBlocks], ids_k[kTileBlocks];   // payload byte offsets
     tile_ids(0, ids_raw);
     to_offs(ids_raw, ids_v);
-    if (n > 0) issue_k(0, ids_v);                      // K(0) for C(-1)
+    if (n > 0 && loader) issue_k(0, ids_v);            // K(0) for C(-1)
     tile_ids(1, ids_raw);
     to_offs(ids_raw, ids_k);
     // Q^T operand fragments (k-step ks: dims 16ks + 8half .. +7 of this lane's row),
@@ -605,11 +614,12 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         ++ph;
     };
     // M(j): softmax of tile j; block ids of tile j+2 (read now, range-checked and
-    // converted at the start of C(j)); then wait for the loads C(j-1) issued.
-    auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+    // converted at the start of C(j)) when this group loads; then wait for the loads
+    // C(j-1) issued.
+    auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks], auto load_tag) {
         // The scalar loads of the ids go out before the softmax, whose length covers
         // their latency (left to itself the scheduler sinks them next to their use).
-        tile_ids(j + 2, ids_raw);
+        if constexpr (decltype(load_tag)::value) tile_ids(j + 2, ids_raw);
         __builtin_amdgcn_sched_barrier(0);
         softmax(j, st, pf);
         wait_vmem();
@@ -622,9 +632,13 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     f32x16 st[2];
     bf16x8 pf[kTileBlocks];
     if (grp == 1) phase_end();
-    if (n > 0) {
+    // The tile loop, instantiated once for a group that loads and once for one that
+    // only reads (row halves, group 1), so that no branch splits a matrix cluster.
+    auto run_tiles = [&](auto load_tag) {
+        constexpr std::true_type T_{};
+        constexpr std::false_type F_{};
         // C(-1): QK(0), loads of V(0) and K(1) (K(1) lands in an unused buffer if n == 1)
-        matrix_cluster(std::false_type{}, std::true_type{}, -1, pf, st, ids_v, ids_k, std::false_type{});
+        matrix_cluster(F_, T_, -1, pf, st, ids_v, ids_k, F_, load_tag);
         phase_end();
         // Four (M, C) pairs per iteration: the scores made in one pair's matrix cluster
         // feed the next pair's softmax in the same registers, and the register copies
@@ -635,34 +649,38 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         for (; j + 4 < n; j += 4) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                vector_cluster(j + u, st, pf);
+                vector_cluster(j + u, st, pf, load_tag);
                 phase_end();
-                matrix_cluster(std::true_type{}, std::true_type{}, j + u, pf, st, ids_v, ids_k, std::true_type{});
+                matrix_cluster(T_, T_, j + u, pf, st, ids_v, ids_k, T_, load_tag);
                 phase_end();
             }
         }
         for (; j + 2 < n; j += 2) {
-            vector_cluster(j, st, pf);
+            vector_cluster(j, st, pf, load_tag);
             phase_end();
-            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k, std::true_type{});
+            matrix_cluster(T_, T_, j, pf, st, ids_v, ids_k, T_, load_tag);
             phase_end();
-            vector_cluster(j + 1, st, pf);
+            vector_cluster(j + 1, st, pf, load_tag);
             phase_end();
-            matrix_cluster(std::true_type{}, std::true_type{}, j + 1, pf, st, ids_v, ids_k, std::true_type{});
+            matrix_cluster(T_, T_, j + 1, pf, st, ids_v, ids_k, T_, load_tag);
             phase_end();
         }
         if (j + 1 < n) {
-            vector_cluster(j, st, pf);
+            vector_cluster(j, st, pf, load_tag);
             phase_end();
-            matrix_cluster(std::true_type{}, std::true_type{}, j, pf, st, ids_v, ids_k, std::true_type{});
+            matrix_cluster(T_, T_, j, pf, st, ids_v, ids_k, T_, load_tag);
             phase_end();
         }
-        vector_cluster(n - 1, st, pf);
+        vector_cluster(n - 1, st, pf, load_tag);
         phase_end();
         // The group's last tile may hold the sequence end: clear V past it.
-        if ((tile_begin + n) * kTileKeys > total) pv(n - 1, pf, std::true_type{});
-        else matrix_cluster(std::true_type{}, std::false_type{}, n - 1, pf, st, ids_v, ids_k, std::false_type{});
+        if ((tile_begin + n) * kTileKeys > total) pv(n - 1, pf, T_);
+        else matrix_cluster(T_, F_, n - 1, pf, st, ids_v, ids_k, F_, load_tag);
         phase_end();
+    };
+    if (n > 0) {
+        if (loader) run_tiles(std::true_type{});
+        else run_tiles(std::false_type{});
     }
     while (ph < phases) phase_end();
 
