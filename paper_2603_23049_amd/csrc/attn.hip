@@ -72,10 +72,12 @@ constexpr int kTileKeys = 64;
 constexpr int kTileBlocks = kTileKeys / kBlockSize;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleThreshold = 8.0f;                // log2 units: P <= 2^8
-// LDS fragment reads kept in flight ahead of the MFMAs in the matrix cluster (5 measured
-// 0.3-0.6% faster than 4, 6, 7 or 8 on the 70B, 8B and RAG-mix shapes).
+// LDS fragment reads kept in flight ahead of the MFMAs in the matrix cluster. With the
+// shared row-halves tiles 3 and 4 measured 0.4-0.8% faster than 5 and 1-2% faster than 6
+// or 7 on the 70B and RAG-mix shapes: the reads are bound by the LDS's throughput, not
+// its latency.
 #ifndef KAHEAD
-#define KAHEAD 5
+#define KAHEAD 4
 #endif
 constexpr int kXcds = 8;                                 // MI355X: 8 XCDs, workgroups dealt round-robin
 

@@ -58,18 +58,26 @@ def test_load_then_append_bitexact(name, mk, method):
 
 
 def test_load_dma_batch_bitexact_or_unsupported():
+    """The batched-copy method is bit-exact where the process's HIP runtime has
+    hipMemcpyBatchAsync; where it has not (the runtime bundled with this PyTorch), the
+    call fails with PCR_ERR_UNSUPPORTED, names the missing call, and queues nothing:
+    the pool still holds its canary bytes."""
     b = synth.tiny()
     data = synth.make_layer(b)
     pk0, pv0 = _canary_pools(b)
     say("[gpu] load dma_batch tiny")
     L = GpuLayer(b, data, pk0, pv0)
+    want_k, want_v = pk0.copy(), pv0.copy()
     try:
         L.load("dma_batch")
     except pcr.PcrError as e:
         assert e.status == pcr.PCR_ERR_UNSUPPORTED
-        pytest.skip("HIP runtime in this process has no hipMemcpyBatchAsync")
+        assert "hipMemcpyBatchAsync" in str(e)
+        torch.cuda.synchronize()
+        assert np.array_equal(u16(L.pool.k), want_k) and np.array_equal(u16(L.pool.v), want_v), \
+            "a refused batched load changed the pool"
+        return
     torch.cuda.synchronize()
-    want_k, want_v = pk0.copy(), pv0.copy()
     odm.load(want_k, want_v, data.host_k, data.host_v, L.src, L.dst)
     assert np.array_equal(u16(L.pool.k), want_k) and np.array_equal(u16(L.pool.v), want_v)
 
