@@ -255,8 +255,9 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
  *   PCR_ATTN_SCHEDULE_KEY_HALVES: 128 packed query rows per workgroup, the two
  *     wave groups on the two halves of the key range, merged at the end;
  *   PCR_ATTN_SCHEDULE_ROW_HALVES: 256 packed query rows per workgroup, each wave
- *     group on 128 of them over the whole key range (half the workgroups, each
- *     with one start-up and no merge for twice the work).
+ *     group on 128 of them over the whole key range, both reading one copy of
+ *     each K/V tile (half the workgroups, each with one start-up and no merge for
+ *     twice the work, and half the tile loads per row).
  * Batches of more than 128 sequences use key halves whatever the setting.
  * Process-wide; takes effect at the next launch. PCR_ERR_INVALID_ARG for an
  * unknown value.
