@@ -93,6 +93,17 @@ pcr_status check_pinned(const void *ptr, int64_t bytes, const char *who, void **
 typedef hipError_t (*memcpy_batch_fn)(void **, void **, size_t *, size_t, hipMemcpyAttributes *, size_t *,
                                       size_t, size_t *, hipStream_t);
 
+// The batched copy takes at least one attribute (the first applying from copy 0):
+// sources read in stream order, no location hints (plain pinned host and device
+// pointers), no flags.
+hipMemcpyAttributes stream_ordered_copy()
+{
+    hipMemcpyAttributes a;
+    memset(&a, 0, sizeof a);
+    a.srcAccessOrder = hipMemcpySrcAccessOrderStream;
+    return a;
+}
+
 memcpy_batch_fn memcpy_batch()
 {
     static memcpy_batch_fn fn = [] {
@@ -359,7 +370,9 @@ pcr_status load_impl(const pcr_host_kv *src, const int32_t *src_blocks, const pc
         if (!batch)
             return fail(PCR_ERR_UNSUPPORTED, "%s: this HIP runtime has no hipMemcpyBatchAsync", who);
         size_t fail_idx = 0;
-        hipError_t e = batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), nullptr, nullptr, 0, &fail_idx, s);
+        hipMemcpyAttributes attr = stream_ordered_copy();
+        size_t attr_first = 0;   // the one attribute applies from copy 0 on
+        hipError_t e = batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), &attr, &attr_first, 1, &fail_idx, s);
         if (e != hipSuccess) return hip_fail(e, "pcr_load_kv_layer: hipMemcpyBatchAsync");
         return PCR_OK;
     }
@@ -512,7 +525,9 @@ pcr_status offload_impl(const pcr_kv_pool *src, const int32_t *src_blocks, const
             }
         }
         size_t fail_idx = 0;
-        hipError_t e = batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), nullptr, nullptr, 0, &fail_idx, s);
+        hipMemcpyAttributes attr = stream_ordered_copy();
+        size_t attr_first = 0;   // the one attribute applies from copy 0 on
+        hipError_t e = batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), &attr, &attr_first, 1, &fail_idx, s);
         if (e != hipSuccess) return hip_fail(e, "pcr_offload_kv_layer: hipMemcpyBatchAsync");
         return PCR_OK;
     }
