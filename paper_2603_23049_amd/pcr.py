@@ -169,6 +169,17 @@ def _i32_host(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
 
 
+def _numel(x) -> int:
+    return int(x.size) if isinstance(x, np.ndarray) else int(x.numel())
+
+
+def _need(x, n: int, what: str):
+    """The library reads device arrays by the lengths it is given, which it cannot check
+    against the allocations: refuse, before the call, a tensor shorter than that."""
+    if x is not None and _numel(x) < n:
+        raise ValueError(f"{what} holds {_numel(x)} elements, the call reads {n}")
+
+
 @dataclass
 class KVPool:
     """One layer's pool: k and v are device tensors of 2-byte elements,
@@ -287,6 +298,10 @@ def staged_workspace_bytes(n_blocks: int, num_kv_heads: int, head_dim: int, bloc
 def append_kv(pool: KVPool, k_new, v_new, slot_mapping, stream=None):
     """pcr_append_kv: k_new/v_new [T][Hkv][d] and slot_mapping [T] are device tensors."""
     T = int(k_new.shape[0])
+    row = pool.num_kv_heads * pool.head_dim
+    _need(k_new, T * row, "k_new")
+    _need(v_new, T * row, "v_new")
+    _need(slot_mapping, T, "slot_mapping")
     p = pool.c()
     _check(lib().pcr_append_kv(ctypes.byref(p), _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), T, _stream(stream)))
 
@@ -301,6 +316,12 @@ def prefix_prefill_attn(q, pool: KVPool, block_tables, prefix_lens, cu_suffix, h
         raise ValueError("host_cu_suffix must have B+1 entries")
     if sm_scale is None:
         sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    T = int(hcu[-1]) if B > 0 else 0
+    _need(q, T * int(num_q_heads) * pool.head_dim, "q")
+    _need(out, T * int(num_q_heads) * pool.head_dim, "out")
+    _need(block_tables, B * int(block_tables.shape[1]), "block_tables")
+    _need(prefix_lens, B, "prefix_lens")
+    _need(cu_suffix, B + 1, "cu_suffix")
     p = pool.c()
     _check(lib().pcr_prefix_prefill_attn(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
                                          _ptr(prefix_lens), _ptr(cu_suffix), _ptr(hpl), _ptr(hcu), B,
@@ -325,6 +346,13 @@ def prefill_attn_set_schedule(schedule: str = "auto"):
     _check(lib().pcr_prefill_attn_set_schedule(ATTN_SCHEDULES[schedule]))
 
 
+def _decode_need(q, out, block_tables, context_lens, B: int, num_q_heads: int, pool: "KVPool"):
+    _need(q, B * int(num_q_heads) * pool.head_dim, "q")
+    _need(out, B * int(num_q_heads) * pool.head_dim, "out")
+    _need(block_tables, B * int(block_tables.shape[1]), "block_tables")
+    _need(context_lens, B, "context_lens")
+
+
 def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, num_q_heads: int, out,
                 workspace=None, sm_scale: Optional[float] = None, stream=None):
     """pcr_decode_attn. q/out [B][Hq][d], block_tables [B][max_blocks], context_lens [B] on the
@@ -335,6 +363,7 @@ def decode_attn(q, pool: KVPool, block_tables, context_lens, host_context_lens, 
     B = int(hcl.shape[0])
     if sm_scale is None:
         sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    _decode_need(q, out, block_tables, context_lens, B, num_q_heads, pool)
     if workspace is None and B > 0:
         import torch
         n = decode_attn_workspace_bytes(B, num_q_heads, pool.num_kv_heads, pool.head_dim, int(hcl.max()))
@@ -362,6 +391,7 @@ def decode_attn_noalloc(q, pool: KVPool, block_tables, context_lens, host_contex
     B = int(hcl.shape[0])
     if sm_scale is None:
         sm_scale = 1.0 / float(np.sqrt(pool.head_dim))
+    _decode_need(q, out, block_tables, context_lens, B, num_q_heads, pool)
     p = pool.c()
     _check(lib().pcr_decode_attn_noalloc(_ptr(q), ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]),
                                          _ptr(context_lens), _ptr(hcl), B, int(num_q_heads), float(sm_scale),
@@ -371,6 +401,11 @@ def decode_attn_noalloc(q, pool: KVPool, block_tables, context_lens, host_contex
 def gather_kv(pool: KVPool, block_tables, starts, cu_out, total: int, k_out, v_out, stream=None):
     """pcr_gather_kv: rows of k_out/v_out [total][Hkv][d] from the pool in logical order."""
     B = int(starts.shape[0])
+    row = pool.num_kv_heads * pool.head_dim
+    _need(cu_out, B + 1, "cu_out")
+    _need(block_tables, B * int(block_tables.shape[1]), "block_tables")
+    _need(k_out, int(total) * row, "k_out")
+    _need(v_out, int(total) * row, "v_out")
     p = pool.c()
     _check(lib().pcr_gather_kv(ctypes.byref(p), _ptr(block_tables), int(block_tables.shape[1]), _ptr(starts),
                                _ptr(cu_out), B, int(total), _ptr(k_out), _ptr(v_out), _stream(stream)))
@@ -404,10 +439,32 @@ class BatchPlan:
         self._keep = (_i32_host(self.src_blocks), _i32_host(self.dst_blocks), _i32_host(self.host_prefix_lens),
                       _i32_host(self.host_cu_suffix))
         sb, db, hpl, hcu = self._keep
+        B = int(hpl.shape[0])
+        if hcu.shape[0] != B + 1:
+            raise ValueError("host_cu_suffix must have B+1 entries")
+        _need(self.slot_mapping, int(hcu[-1]) if B > 0 else 0, "slot_mapping")
+        _need(self.block_tables, B * int(self.block_tables.shape[1]), "block_tables")
+        _need(self.prefix_lens, B, "prefix_lens")
+        _need(self.cu_suffix, B + 1, "cu_suffix")
         return _Batch(_ptr(sb), _ptr(db), int(sb.shape[0]), _ptr(self.slot_mapping), int(self.slot_mapping.shape[0]),
                       _ptr(self.block_tables), int(self.block_tables.shape[1]), _ptr(self.prefix_lens),
                       _ptr(self.cu_suffix), _ptr(hpl), _ptr(hcu), int(hpl.shape[0]), int(self.num_q_heads),
                       float(self.sm_scale))
+
+
+def _layers_io(layers: Sequence[Layer], batch: BatchPlan):
+    """The layer array of the pipeline calls, each layer's device tensors checked against
+    the lengths the batch makes the library read."""
+    T = int(_i32_host(batch.host_cu_suffix)[-1])
+    arr = (_LayerIO * max(len(layers), 1))()
+    for i, L in enumerate(layers):
+        d, hkv = L.pool.head_dim, L.pool.num_kv_heads
+        _need(L.q, T * int(batch.num_q_heads) * d, f"layer {i} q")
+        _need(L.out, T * int(batch.num_q_heads) * d, f"layer {i} out")
+        _need(L.k_new, T * hkv * d, f"layer {i} k_new")
+        _need(L.v_new, T * hkv * d, f"layer {i} v_new")
+        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    return arr
 
 
 def pipeline_run(layers: Sequence[Layer], batch: BatchPlan, copy_stream, compute_stream, method: str = "auto",
@@ -415,9 +472,7 @@ def pipeline_run(layers: Sequence[Layer], batch: BatchPlan, copy_stream, compute
     """pcr_pipeline_run. With timing=True, waits for the last layer and returns a dict of
     per-layer load/compute/wait ms and totals; otherwise only enqueues and returns None."""
     n = len(layers)
-    arr = (_LayerIO * max(n, 1))()
-    for i, L in enumerate(layers):
-        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    arr = _layers_io(layers, batch)
     b = batch.c()
     t = np.zeros(4 * n + 2, np.float32) if timing else None
     _check(lib().pcr_pipeline_run(arr, n, ctypes.byref(b), LOAD_METHODS[method], _stream(copy_stream),
@@ -437,9 +492,7 @@ def pipeline_run_staged(layers: Sequence[Layer], batch: BatchPlan, workspace, co
     beyond the first let the next transfer run during a scatter. Timing as
     pipeline_run."""
     n = len(layers)
-    arr = (_LayerIO * max(n, 1))()
-    for i, L in enumerate(layers):
-        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    arr = _layers_io(layers, batch)
     b = batch.c()
     t = np.zeros(4 * n + 2, np.float32) if timing else None
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
@@ -457,13 +510,11 @@ def pipeline_staged_slot_bytes(n_pairs: int, num_kv_heads: int, head_dim: int, b
     return staged_workspace_bytes(n_pairs, num_kv_heads, head_dim, block_size)
 
 
-def _offload_args(layers, offload_dst, off_src, off_dst):
+def _offload_args(layers, batch, offload_dst, off_src, off_dst):
     n = len(layers)
     if len(offload_dst) != n:
         raise ValueError("one offload destination per layer")
-    arr = (_LayerIO * max(n, 1))()
-    for i, L in enumerate(layers):
-        arr[i] = _LayerIO(L.host.c(), L.pool.c(), _ptr(L.q), _ptr(L.k_new), _ptr(L.v_new), _ptr(L.out))
+    arr = _layers_io(layers, batch)
     dst = (_Host * max(n, 1))()
     for i, h in enumerate(offload_dst):
         dst[i] = h.c()
@@ -489,7 +540,7 @@ def pipeline_run_offload(layers: Sequence[Layer], offload_dst: Sequence[HostKV],
                          offload_method: str = "auto", workspace=None, timing: bool = False):
     """pcr_pipeline_run_offload: the three-stream pipeline. With timing=True, waits for the
     last offload and returns per-layer load/compute/wait/offload ms and totals."""
-    n, arr, dst, sb, db = _offload_args(layers, offload_dst, off_src, off_dst)
+    n, arr, dst, sb, db = _offload_args(layers, batch, offload_dst, off_src, off_dst)
     b = batch.c()
     t = np.zeros(6 * n + 3, np.float32) if timing else None
     _check(lib().pcr_pipeline_run_offload(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
@@ -505,7 +556,7 @@ def pipeline_run_offload_staged(layers: Sequence[Layer], offload_dst: Sequence[H
     """pcr_pipeline_run_offload_staged: the offload pipeline with staged loads (four
     streams). load_workspace as pipeline_run_staged's workspace; offload_workspace as
     pipeline_run_offload's. Timing as pipeline_run_offload."""
-    n, arr, dst, sb, db = _offload_args(layers, offload_dst, off_src, off_dst)
+    n, arr, dst, sb, db = _offload_args(layers, batch, offload_dst, off_src, off_dst)
     b = batch.c()
     t = np.zeros(6 * n + 3, np.float32) if timing else None
     _check(lib().pcr_pipeline_run_offload_staged(arr, dst, n, ctypes.byref(b), _ptr(sb), _ptr(db), int(sb.shape[0]),
