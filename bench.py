@@ -320,7 +320,7 @@ def warm_up(fn, min_ms, min_calls=3):
                 return n
 
 
-def measure_step(batch, steps, warmup, min_warm_ms=500.0):
+def measure_step(batch, steps, warmup, min_warm_ms=500.0, graph=True):
     """Timed compute step (append + attention) with prefix KV already in the pool.
 
     Warm-up: `warmup` steps, then more until at least min_warm_ms of sustained work has
@@ -329,7 +329,8 @@ def measure_step(batch, steps, warmup, min_warm_ms=500.0):
     synchronized on both sides; inside it each attention launch is bracketed by its own
     event pair on the stream it runs on, so the attention's per-launch time comes from
     the same window as the step time. Then the append alone, back to back, for its
-    per-launch time (a launch-bound kernel at these sizes)."""
+    per-launch time (a launch-bound kernel at these sizes), the attention alone back to
+    back, and (graph=True) the step replayed from a HIP graph."""
     import torch
     from paper_2603_23049_amd import pcr
     L, bp, _ = _setup_layer(batch)
@@ -377,10 +378,47 @@ def measure_step(batch, steps, warmup, min_warm_ms=500.0):
         _attn(L, bp, s)
     e3.record(s)
     e3.synchronize()
+    graph_ms = _graph_step_ms(L, bp, steps) if graph else None
     return dict(step_ms=float(step_ms), wall_ms_per_step=wall / steps * 1e3, append_ms=append_ms,
+                graph_step_ms=graph_ms,
                 attn_ms=attn_ms, attn_ms_min=float(min(launches)), attn_ms_max=float(max(launches)),
                 attn_ms_median=_median(launches), attn_b2b_ms=a3.elapsed_time(e3) / steps, wall_s=wall,
                 warmup_calls=warmup + warm_calls)
+
+
+def _graph_step_ms(L, bp, steps):
+    """The compute step (append + attention) captured once into a HIP graph (torch's
+    CUDAGraph: the library's launches on the capturing stream become its nodes) and
+    replayed `steps` times back to back under one event pair: the step without the host
+    launch gaps between its kernels."""
+    import torch
+    from paper_2603_23049_amd import pcr
+
+    def step():   # on the current stream (the capturing one inside the graph context)
+        pcr.append_kv(L.pool, L.k_new, L.v_new, bp.slot_mapping)
+        _attn(L, bp)
+
+    s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(s)
+    with torch.cuda.stream(side):    # one eager step on a side stream before capture
+        step()
+    s.wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    g.replay()
+    torch.cuda.synchronize()
+    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(steps):
+        g.replay()
+    e.record(s)
+    e.synchronize()
+    ms = a.elapsed_time(e) / steps
+    del g
+    return float(ms)
 
 
 def measure_load(batch, reps=10):
@@ -972,7 +1010,9 @@ def _step_record(batch, st):
             "step_tflops": flops / (st["step_ms"] * 1e-3) / 1e12,
             "attn_tflops": flops / (st["attn_b2b_ms"] * 1e-3) / 1e12,
             "attn_frac": flops / (st["attn_b2b_ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
-            "attn_timing": "back to back, one event pair over the launches", "warmup_calls": st["warmup_calls"]}
+            "attn_timing": "back to back, one event pair over the launches", "warmup_calls": st["warmup_calls"],
+            "graph_ms_per_step": st["graph_step_ms"],
+            "graph_step_tflops": flops / (st["graph_step_ms"] * 1e-3) / 1e12 if st["graph_step_ms"] else None}
 
 
 def _main(args, sampler):
@@ -1019,7 +1059,9 @@ def _main(args, sampler):
     batch = workload(args.workload)
     flops = attention_flops(batch.prefix_lens, batch.suffix_lens, batch.num_q_heads, batch.head_dim)
     _say(f"[bench] step: {args.workload} warmup={args.warmup} (+ at least 500 ms) steps={args.steps}")
-    st = measure_step(batch, args.steps, args.warmup)
+    # (no graph replays in the profiled run: its trace's timed window is the attention
+    # dispatches before the last 20)
+    st = measure_step(batch, args.steps, args.warmup, graph=not args.step_only)
     value = flops / (st["step_ms"] * 1e-3) / 1e12
     attn_tflops = flops / (st["attn_ms"] * 1e-3) / 1e12
     app_b = append_bytes(batch.T, batch.num_kv_heads, batch.head_dim)
@@ -1179,6 +1221,7 @@ def _main(args, sampler):
         "cpu_baseline_legs": legs,
         "wall_s_timed": st["wall_s"],
         "wall_ms_per_step": st["wall_ms_per_step"],
+        "graph_ms_per_step": st["graph_step_ms"],
     }
     rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "prefetch",
                                           "append_sweep", "hit_ratio")})
