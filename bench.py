@@ -888,25 +888,26 @@ def hit_ratio_report(capacities=(64, 128, 200, 300), n_requests=400):
     return out
 
 
-def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8, d=128, reps=20):
+def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8, d=128, reps=20,
+                         ragged_seq=300):
     """The scatter (pcr_append_kv) from 1k to 128k new tokens (8 MiB to 1 GiB of K+V
     moved: every row read once and written once), each size timed back to back after a
-    warm-up; the pool holds exactly the tokens' blocks in a random order."""
+    warm-up, for two slot lists: `sizes`, the tokens in block order over a random order
+    of the pool's blocks (every 8-slot chunk of V aligned with the workgroups' tiles);
+    `ragged`, sequences of `ragged_seq` new tokens laid end to end, each starting at a
+    block of its own (random blocks), so that the tiles of the token stream start
+    inside the sequences' chunks, as in a ragged batch."""
     import torch
     from paper_2603_23049_amd import pcr
     bs = 16
     s = torch.cuda.current_stream()
-    out = []
     g = torch.Generator(device="cuda").manual_seed(17)
-    for T in token_counts:
-        nb = -(-T // bs)
+
+    def timed(T, nb, slots):
         pool = pcr.KVPool(torch.zeros((nb, Hkv, bs * d), dtype=torch.int16, device="cuda"),
                           torch.zeros((nb, Hkv, bs * d), dtype=torch.int16, device="cuda"), Hkv, d)
         k = torch.randint(-32768, 32767, (T, Hkv, d), dtype=torch.int16, device="cuda", generator=g)
         v = torch.randint(-32768, 32767, (T, Hkv, d), dtype=torch.int16, device="cuda", generator=g)
-        perm = torch.randperm(nb, device="cuda", generator=g).to(torch.int32)
-        slots = (perm.repeat_interleave(bs)[:T] * bs + torch.arange(T, device="cuda", dtype=torch.int32) % bs)
-        slots = slots.to(torch.int32).contiguous()
         fn = lambda: pcr.append_kv(pool, k, v, slots, stream=s)
         warm_up(fn, 30.0)
         a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -917,9 +918,24 @@ def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8,
         e.synchronize()
         ms = a.elapsed_time(e) / reps
         nbytes = append_bytes(T, Hkv, d)
-        out.append({"T": T, "bytes": nbytes, "ms": ms, "GBps": nbytes / ms / 1e6,
-                    "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS})
-        del pool, k, v, slots, perm
+        del pool, k, v
+        return {"T": T, "bytes": nbytes, "ms": ms, "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS}
+
+    out, ragged = [], []
+    for T in token_counts:
+        nb = -(-T // bs)
+        perm = torch.randperm(nb, device="cuda", generator=g).to(torch.int32)
+        slots = (perm.repeat_interleave(bs)[:T] * bs + torch.arange(T, device="cuda", dtype=torch.int32) % bs)
+        out.append(timed(T, nb, slots.to(torch.int32).contiguous()))
+        per_seq = -(-ragged_seq // bs)
+        n_seq = -(-T // ragged_seq)
+        nbr = n_seq * per_seq
+        blocks = torch.randperm(nbr, device="cuda", generator=g).to(torch.int32)
+        idx = torch.arange(T, device="cuda", dtype=torch.int32)
+        pos = idx % ragged_seq
+        slots_r = blocks[(idx // ragged_seq) * per_seq + pos // bs] * bs + pos % bs
+        ragged.append(timed(T, nbr, slots_r.to(torch.int32).contiguous()))
+        del perm, slots, blocks, slots_r
     torch.cuda.synchronize()
     # reference: a plain device copy of 256 MiB (read + write, like the append)
     src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
@@ -935,7 +951,8 @@ def measure_append_sweep(token_counts=(1024, 4096, 16384, 65536, 131072), Hkv=8,
     copy_gbps = 2 * (256 << 20) / (a.elapsed_time(e) / reps) / 1e6
     del src, dst
     return {"sizes": out, "asymptotic_GBps": out[-1]["GBps"], "asymptotic_frac_hbm": out[-1]["frac_hbm"],
-            "device_copy_256MiB_GBps": copy_gbps, "asymptotic_frac_of_device_copy": out[-1]["GBps"] / copy_gbps}
+            "device_copy_256MiB_GBps": copy_gbps, "asymptotic_frac_of_device_copy": out[-1]["GBps"] / copy_gbps,
+            "ragged": ragged, "ragged_seq_tokens": ragged_seq, "ragged_asymptotic_GBps": ragged[-1]["GBps"]}
 
 
 def main(argv=None):

@@ -209,8 +209,9 @@ pcr_status pcr_load_kv_layer_staged(const pcr_host_kv *src, const int32_t *src_b
  * computing the uncached tokens implies, Sec. 4.3).
  *   k_new, v_new   device, bf16 [T][Hkv][d] (row-major, contiguous)
  *   slot_mapping   device, int32 [T]: pool slot of token t (block*bs + offset);
- *                  slots must be distinct and inside the pool (not re-checked
- *                  on the device: the values live in device memory)
+ *                  slots must be distinct; a token whose slot is negative or
+ *                  outside the pool is skipped by the kernel (no error is
+ *                  reported: the values live in device memory)
  * When a prefix ends inside a block, that block must be loaded before this call
  * (the load copies the whole block; the append then fills its free slots).
  */
