@@ -560,27 +560,35 @@ def measure_pipeline(batch, method, load_ms_iso, compute_ms_iso, reps=3, distinc
             "exposed_ideal_ms_per_layer": load_ms_iso / n if compute_ms_iso >= load_ms_iso else None}
 
 
-def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
-    """One decode step (one new token per sequence, attending over ctx keys) of a
-    Llama-3-8B-shaped batch, attention only, through the split-key decode entry point;
-    the prefill kernel on the same rows (one-token suffixes) is timed beside it. Pool, Q
-    and tables drawn on the device (the values do not change the work). HBM bytes =
-    every key's K and V once + Q + out."""
+def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71, name=None, prefill_beside=True):
+    """One decode step (one new token per sequence, attending over its context) of a
+    Llama-3-8B-shaped batch, attention only, through the split-key decode entry point
+    with the workspace its size query asks for; `ctx` is one length for every sequence
+    or one per sequence (ragged). The prefill kernel on the same rows (one-token
+    suffixes) is timed beside it. Pool, Q and tables drawn on the device (the values do
+    not change the work). HBM bytes = every key's K and V once + Q + out."""
     import torch
     from paper_2603_23049_amd import pcr
     bs = 16
-    nb = -(-ctx // bs)
+    n_h = np.asarray(ctx, np.int32) if np.ndim(ctx) else np.full(B, ctx, np.int32)
+    B = int(n_h.shape[0])
+    nbs = -(-n_h // bs)
+    mb = int(nbs.max())
     g = torch.Generator(device="cuda").manual_seed(seed)
-    pool_blocks = B * nb
+    pool_blocks = int(nbs.sum())
     pk = torch.randn((pool_blocks, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
     pv = torch.randn((pool_blocks, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
     pool = pcr.KVPool(pk, pv, Hkv, d)
-    bt = torch.randperm(pool_blocks, device="cuda", generator=g).to(torch.int32).view(B, nb)
+    perm = torch.randperm(pool_blocks, device="cuda", generator=g).to(torch.int32).cpu().numpy()
+    bt_h = np.full((B, mb), -1, np.int32)
+    off = np.concatenate([[0], np.cumsum(nbs)])
+    for b in range(B):
+        bt_h[b, :nbs[b]] = perm[off[b]:off[b + 1]]
+    bt = torch.from_numpy(bt_h).cuda()
     q = torch.randn((B, Hq, d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
     out = torch.empty_like(q)
-    n_h = np.full(B, ctx, np.int32)
     n_d = torch.from_numpy(n_h).cuda()
-    ws_bytes = pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, ctx)
+    ws_bytes = pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, int(n_h.max()))
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
     pl_h = n_h - 1
     cu_h = np.arange(B + 1, dtype=np.int32)
@@ -598,12 +606,29 @@ def measure_decode(B=64, ctx=4352, Hq=32, Hkv=8, d=128, steps=30, seed=71):
         return a.elapsed_time(e) / steps
 
     ms = timed(lambda: pcr.decode_attn(q, pool, bt, n_d, n_h, Hq, out, workspace=ws, stream=s))
-    ms_prefill = timed(lambda: pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s))
-    nbytes = B * ctx * Hkv * d * 2 * 2 + 2 * B * Hq * d * 2
-    return {"workload": f"decode B={B} ctx={ctx} Hq={Hq} Hkv={Hkv} d={d}", "attn_ms": ms, "hbm_bytes": nbytes,
-            "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3,
-            "workspace_bytes": ws_bytes, "prefill_kernel_ms": ms_prefill,
-            "prefill_kernel_frac_hbm": nbytes / ms_prefill / 1e6 / HBM_PEAK_GBS}
+    ms_prefill = timed(lambda: pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)) \
+        if prefill_beside else None
+    keys = int(n_h.sum())
+    nbytes = keys * Hkv * d * 2 * 2 + 2 * B * Hq * d * 2
+    label = name or f"decode B={B} ctx={int(n_h[0]) if np.all(n_h == n_h[0]) else 'ragged'} Hq={Hq} Hkv={Hkv} d={d}"
+    rec = {"workload": label, "keys": keys, "max_context": int(n_h.max()), "attn_ms": ms, "hbm_bytes": nbytes,
+           "GBps": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / HBM_PEAK_GBS, "tokens_per_s": B / ms * 1e3,
+           "workspace_bytes": ws_bytes}
+    if ms_prefill is not None:
+        rec.update(prefill_kernel_ms=ms_prefill, prefill_kernel_frac_hbm=nbytes / ms_prefill / 1e6 / HBM_PEAK_GBS)
+    return rec
+
+
+def measure_decode_ragged():
+    """Decode steps of ragged batches: 64 sequences with contexts drawn uniformly from
+    1024-8192 keys (seed 3), and the RAG mix's 16 requests at their full contexts (the
+    decode of the requests the prefill step served)."""
+    rng = np.random.default_rng(3)
+    rag = workload("rag_mix")
+    return [measure_decode(ctx=rng.integers(1024, 8193, 64).astype(np.int32), name="decode B=64 ctx 1k-8k ragged",
+                           prefill_beside=False),
+            measure_decode(ctx=(np.asarray(rag.prefix_lens) + np.asarray(rag.suffix_lens)).astype(np.int32),
+                           name="decode RAG mix 16 requests", prefill_beside=False)]
 
 
 def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_sweep=(48, 96, 192), request_compute_ms=30.0,
@@ -1043,7 +1068,7 @@ def _main(args, sampler):
         copy_calibration()
         return 0
     if args.decode_only:
-        print(json.dumps({"decode": measure_decode()}), flush=True)
+        print(json.dumps({"decode": measure_decode(), "decode_ragged": measure_decode_ragged()}), flush=True)
         return 0
     if args.append_sweep_only:
         print(json.dumps({"append_sweep": measure_append_sweep()}), flush=True)
@@ -1169,6 +1194,7 @@ def _main(args, sampler):
         extra["prefetch"] = measure_prefetch()
         _say("[bench] decode step")
         extra["decode"] = measure_decode()
+        extra["decode_ragged"] = measure_decode_ragged()
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
         rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=200.0)
@@ -1240,7 +1266,7 @@ def _main(args, sampler):
         "wall_ms_per_step": st["wall_ms_per_step"],
         "graph_ms_per_step": st["graph_step_ms"],
     }
-    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "prefetch",
+    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "decode_ragged", "prefetch",
                                           "append_sweep", "hit_ratio")})
     print(json.dumps(rec), flush=True)
     return 0

@@ -282,14 +282,21 @@ pcr_status pcr_prefill_attn_set_schedule(int32_t schedule);
  *                      (sizes the launch; the two must be equal)
  *   out                device bf16 [B][Hq][d], 16-byte aligned; fp32 accumulation,
  *                      rounded to nearest even
- *   workspace          device memory owned by the caller, 16-byte aligned, of at least
+ *   workspace          device memory owned by the caller, 16-byte aligned, of
  *                      pcr_decode_attn_workspace_size(B, Hq, Hkv, d, max_b n_b) bytes
  *                      (NULL when that is 0); its contents are scratch. One workspace
  *                      serves every call ordered on one stream; calls that may overlap
  *                      need their own.
  * The key range of each (sequence, kv head) is split into chunks processed in
- * parallel and merged exactly (a second kernel on the same stream), so the
- * result does not depend on the split beyond fp32 rounding. Numerics as for
+ * parallel and merged exactly (in LDS, or through the workspace and a second
+ * kernel on the same stream), so the result does not depend on the split beyond
+ * fp32 rounding. The chunk size follows the total count of keys when that gives
+ * shorter chunks than the largest context alone (ragged batches: long sequences
+ * get more chunks than short ones) and the workspace holds that plan; otherwise
+ * it follows the largest context, which needs at most the workspace that
+ * pcr_decode_attn_workspace_size reported before ragged plans existed (the error
+ * message names the size needed). The plan depends only on the host context
+ * lengths and the workspace size, so repeated calls give identical bits. Numerics as for
  * pcr_prefix_prefill_attn (fp32 scores, bf16 probabilities, rows normalised by
  * the rounded values); sm_scale must be finite and > 0.
  * Errors: PCR_ERR_UNSUPPORTED if Hq/Hkv > 16 (pcr_prefix_prefill_attn with
@@ -310,6 +317,8 @@ pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t
  * scratch array of PCR_DECODE_NOALLOC_SCRATCH_BYTES (16 MiB) that the library
  * holds per device until the process ends (its address is taken on the first call
  * on each device). The call allocates nothing and calls no allocating routine.
+ * With a workspace of pcr_decode_attn_workspace_size bytes, pcr_decode_attn makes
+ * the same plan as this entry point and gives the same bits.
  * Every call on one device shares that device's scratch, which keeps the last
  * call's contents (nothing needs clearing: each call writes every entry it reads
  * back), so calls on one device that may overlap (different streams, or host
@@ -326,10 +335,13 @@ pcr_status pcr_decode_attn_noalloc(const void *q, const pcr_kv_pool *pool, const
                                    float sm_scale, void *out, void *stream);
 
 /*
- * pcr_decode_attn_workspace_size -- bytes of workspace pcr_decode_attn needs on the
- * current device for any batch of B sequences whose context lengths are at most
- * max_context (0 when every such batch is handled without one). Queries the
- * device's compute-unit count; PCR_ERR_HIP when no device is usable.
+ * pcr_decode_attn_workspace_size -- bytes of workspace with which pcr_decode_attn
+ * takes its best plan on the current device for any batch of B sequences whose
+ * context lengths are at most max_context (0 when every such batch is handled
+ * without one); never decreases as max_context grows, and never exceeds
+ * PCR_DECODE_NOALLOC_SCRATCH_BYTES beyond what the plan by the largest context
+ * needs. Queries the device's compute-unit count; PCR_ERR_HIP when no device is
+ * usable.
  */
 pcr_status pcr_decode_attn_workspace_size(int32_t B, int32_t num_q_heads, int32_t num_kv_heads,
                                           int32_t head_dim, int32_t max_context, int64_t *bytes);

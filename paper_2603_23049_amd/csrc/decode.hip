@@ -356,22 +356,63 @@ hipError_t decode_noalloc_scratch(void **ptr)
 }
 
 DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                       int32_t max_context, int32_t n_cu)
+                       int32_t max_context, int32_t n_cu, const int32_t *ctx, int64_t ws_limit)
 {
     DecodePlan p{};
     const int64_t pairs = (int64_t)B * num_kv_heads;
     if (pairs <= 0 || max_context <= 0) return p;
-    const int64_t want = ((int64_t)n_cu * waves_per_cu(head_dim) + pairs - 1) / pairs;
-    const int64_t cap = ((int64_t)max_context + kMinChunk - 1) / kMinChunk;
-    const int64_t bound = std::max<int64_t>(1, std::min(want, cap));
-    int64_t chunk = ((int64_t)max_context + bound - 1) / bound;
-    chunk = (chunk + kStepKeys - 1) / kStepKeys * kStepKeys;
     const int64_t G = num_q_heads / num_kv_heads;
-    p.bound_split = (int32_t)bound;
+    const int64_t part_bytes = G * (head_dim + 2) * 4;      // one chunk's O, max and sum per query head
+    const int64_t waves = (int64_t)n_cu * waves_per_cu(head_dim);
+    const int64_t want = (waves + pairs - 1) / pairs;      // chunks per sequence that fill the SIMDs
+    const int64_t cap = ((int64_t)max_context + kMinChunk - 1) / kMinChunk;
+    auto round_chunk = [](int64_t c) { return (c + kStepKeys - 1) / kStepKeys * kStepKeys; };
+    // Rule by the largest context: every sequence gets up to `bound` chunks of equal size.
+    const int64_t bound = std::max<int64_t>(1, std::min(want, cap));
+    const int64_t chunk = round_chunk(((int64_t)max_context + bound - 1) / bound);
     p.chunk = (int32_t)chunk;
     p.n_split = (int32_t)(((int64_t)max_context + chunk - 1) / chunk);
-    p.workspace_bytes = p.n_split > kWaves ? pairs * p.n_split * G * (head_dim + 2) * 4 : 0;
-    p.bound_workspace_bytes = bound > kWaves ? pairs * bound * G * (head_dim + 2) * 4 : 0;
+    p.lds_merge = p.n_split > 1 && p.n_split <= kWaves;
+    p.ws_wg_waves = kWaves;
+    p.workspace_bytes = p.n_split > kWaves ? pairs * p.n_split * part_bytes : 0;
+    // Rule by the total count of keys (ragged batches; only when the sequences alone do
+    // not fill the SIMDs): the smallest chunk whose chunks over all sequences still give
+    // at most one wave per SIMD, with up to 2 * want chunks for the longest sequence.
+    const int64_t s_max = want > 1 ? std::min(cap, 2 * want) : 1;
+    const int64_t bound_old = bound > kWaves ? pairs * bound * part_bytes : 0;
+    // (a plan by total keys needing more than the allocation-free scratch is never taken)
+    p.bound_workspace_bytes =
+        std::max(bound_old, s_max > 1 ? std::min<int64_t>(pairs * s_max * part_bytes, kDecodeScratchBytes) : 0);
+    if (!ctx || s_max <= 1) return p;
+    auto active = [&](int64_t c) {
+        int64_t n = 0;
+        for (int32_t b = 0; b < B; ++b) n += ((int64_t)ctx[b] + c - 1) / c;
+        return n * num_kv_heads;
+    };
+    int64_t lo = round_chunk(std::max<int64_t>(kMinChunk, ((int64_t)max_context + s_max - 1) / s_max));
+    int64_t hi = chunk;
+    if (lo >= hi || active(hi) > waves) return p;
+    while (lo < hi) {   // smallest chunk (a multiple of kStepKeys) with active(chunk) <= waves
+        const int64_t mid = round_chunk((lo + hi) / 2);
+        if (mid >= hi) break;
+        if (active(mid) <= waves) hi = mid; else lo = mid + kStepKeys;
+    }
+    const int64_t c2 = hi;
+    if (c2 >= chunk) return p;
+    const int64_t n2 = ((int64_t)max_context + c2 - 1) / c2;
+    bool full = true;   // every sequence has all n2 chunks: they can merge in LDS
+    for (int32_t b = 0; b < B && full; ++b) full = ((int64_t)ctx[b] + c2 - 1) / c2 == n2;
+    const bool lds = n2 > 1 && n2 <= kWaves && full;
+    const int64_t ws = (n2 > 1 && !lds) ? pairs * n2 * part_bytes : 0;
+    if (ws > ws_limit) return p;
+    p.chunk = (int32_t)c2;
+    p.n_split = (int32_t)n2;
+    p.lds_merge = lds;
+    // One wave per workgroup: chunks past a short sequence's end then end their own
+    // workgroup at once and leave the SIMD to another chunk (a wave takes a whole SIMD,
+    // so a four-wave workgroup holds a compute unit until its longest chunk is done).
+    p.ws_wg_waves = 1;
+    p.workspace_bytes = ws;
     return p;
 }
 
@@ -383,11 +424,12 @@ hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int3
 {
     const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv, D = pool.head_dim;
     const int64_t n_tasks = (int64_t)B * Hkv * plan.n_split;
-    // Up to kWaves chunks of a sequence share one workgroup and merge in LDS; more go
-    // through the workspace and decode_combine_kernel.
-    const bool through_ws = plan.n_split > kWaves;
-    const int lds_merge = plan.n_split > 1 && !through_ws;
-    const int wg_waves = through_ws ? kWaves : plan.n_split;
+    // Up to kWaves chunks of a sequence share one workgroup and merge in LDS when every
+    // sequence has all n_split of them; otherwise they go through the workspace and
+    // decode_combine_kernel (a chunk past its sequence's end then ends its wave at once).
+    const int lds_merge = plan.lds_merge;
+    const bool through_ws = plan.n_split > 1 && !lds_merge;
+    const int wg_waves = through_ws ? plan.ws_wg_waves : plan.n_split;
     const dim3 grid((unsigned)((n_tasks + wg_waves - 1) / wg_waves));
     const size_t lds = lds_merge ? (size_t)wg_waves * 64 * ((D / 16) * 16 + 8) : 0;
     float *ws_o = through_ws ? static_cast<float *>(workspace) : nullptr;

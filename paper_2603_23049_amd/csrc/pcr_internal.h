@@ -52,18 +52,25 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
 pcr_status device_cu_count(int32_t *n_cu, const char *who);
 
 // Decode attention (decode.hip). The key range of each (sequence, kv head) is cut
-// into n_split chunks of `chunk` keys; bound_split is the split count for the
-// largest context the plan was made for, an upper bound of n_split for every
-// smaller one (the workspace sizes follow the two counts).
+// into chunks of `chunk` keys, at most n_split per sequence. Without the context
+// lengths (or when it does not shorten the chunks) the chunk follows from the
+// largest context; with them, from the total count of keys (a ragged batch then
+// gives its long sequences more chunks than its short ones). lds_merge: every
+// sequence has n_split <= 4 chunks and they merge in LDS; otherwise chunks of one
+// sequence merge through the workspace. bound_workspace_bytes covers every batch of
+// B sequences with contexts up to max_context, under either rule.
 struct DecodePlan {
     int32_t n_split;
     int32_t chunk;
-    int32_t bound_split;
+    int32_t lds_merge;
+    int32_t ws_wg_waves;   // waves per workgroup when chunks merge through the workspace
     int64_t workspace_bytes;
     int64_t bound_workspace_bytes;
 };
+// ctx: the host context lengths (NULL: plan from max_context alone); the rule by total
+// keys is taken only when its workspace fits ws_limit bytes.
 DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                       int32_t max_context, int32_t n_cu);
+                       int32_t max_context, int32_t n_cu, const int32_t *ctx = nullptr, int64_t ws_limit = 0);
 int decode_max_cols();
 hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int32_t *block_tables,
                               int32_t max_blocks, const int32_t *context_lens, int32_t B, int32_t num_q_heads,

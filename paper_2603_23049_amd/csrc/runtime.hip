@@ -718,8 +718,8 @@ pcr_status pcr_decode_attn_workspace_size(int32_t B, int32_t num_q_heads, int32_
 // (plan->n_split == 0: nothing to do).
 static pcr_status decode_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
                                int32_t max_blocks, const int32_t *context_lens, const int32_t *host_context_lens,
-                               int32_t B, int32_t num_q_heads, float sm_scale, const void *out, const char *who,
-                               DecodePlan *plan)
+                               int32_t B, int32_t num_q_heads, float sm_scale, const void *out, int64_t ws_limit,
+                               const char *who, DecodePlan *plan)
 {
     *plan = DecodePlan{};
     pcr_status st = check_pool(pool, who);
@@ -749,7 +749,8 @@ static pcr_status decode_check(const void *q, const pcr_kv_pool *pool, const int
     int32_t n_cu = 0;
     st = device_cu_count(&n_cu, who);
     if (st) return st;
-    *plan = decode_plan(B, num_q_heads, pool->num_kv_heads, pool->head_dim, max_ctx, n_cu);
+    *plan = decode_plan(B, num_q_heads, pool->num_kv_heads, pool->head_dim, max_ctx, n_cu, host_context_lens,
+                        ws_limit);
     return PCR_OK;
 }
 
@@ -764,7 +765,7 @@ pcr_status pcr_decode_attn_noalloc(const void *q, const pcr_kv_pool *pool, const
     const char *who = "pcr_decode_attn_noalloc";
     DecodePlan plan;
     pcr_status st = decode_check(q, pool, block_tables, max_blocks, context_lens, host_context_lens, B, num_q_heads,
-                                 sm_scale, out, who, &plan);
+                                 sm_scale, out, kDecodeScratchBytes, who, &plan);
     if (st || plan.n_split == 0) return st;
     void *ws = nullptr;
     if (plan.workspace_bytes > 0) {
@@ -789,8 +790,12 @@ pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t
     g_err[0] = 0;
     const char *who = "pcr_decode_attn";
     DecodePlan plan;
+    // The plan by total keys is taken when its workspace fits the one given and the
+    // allocation-free entry point's scratch, so that both entry points make the same plan
+    // for a batch whenever the workspace holds pcr_decode_attn_workspace_size bytes.
+    const int64_t ws_limit = workspace ? std::min<int64_t>(workspace_bytes, kDecodeScratchBytes) : 0;
     pcr_status st = decode_check(q, pool, block_tables, max_blocks, context_lens, host_context_lens, B, num_q_heads,
-                                 sm_scale, out, who, &plan);
+                                 sm_scale, out, ws_limit, who, &plan);
     if (st || plan.n_split == 0) return st;
     if (plan.workspace_bytes > 0) {
         if (!workspace || workspace_bytes < plan.workspace_bytes)

@@ -80,18 +80,53 @@ def test_decode_ragged_contexts(Hq, Hkv, d):
 
 @pytest.mark.parametrize("B,d", [(32, 128), (48, 128), (100, 128), (32, 64)])
 def test_decode_ragged_merged_in_workgroup(B, d):
-    """Batches whose sequences are cut into 2-4 chunks merged inside one workgroup (no
-    workspace): ragged contexts, so some chunks lie past a short sequence's end."""
+    """Batches whose sequences are cut into 2-4 chunks merged inside one workgroup: the
+    plan by the largest context, which needs no workspace (a one-byte workspace is
+    given, too small for the plan by total keys); ragged contexts, so some chunks lie
+    past a short sequence's end. Then the same batch with the workspace the size query
+    asks for, which takes the plan by total keys (chunks merged through the workspace)."""
     Hq, Hkv = 32, 8
     rng = np.random.Generator(np.random.PCG64(B + d))
     ctx = [int(x) for x in rng.integers(1, 4353, B)]
     ctx[:6] = [1, 16, 33, 1100, 2200, 4352]
-    assert pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, max(ctx)) == 0
     q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=B * 3 + d)
+    want = _decode_oracle(q, pk, pv, bt, ctx, Hkv)
     say(f"[gpu] decode merged in workgroup B={B} d={d}")
+    tiny = torch.empty(1, dtype=torch.uint8, device="cuda")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=tiny)
+    _check(synth.bf16_bits_to_f32(u16(out)).astype(np.float64), want, f"decode merged B={B} d={d}")
+    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    _check(synth.bf16_bits_to_f32(u16(out)).astype(np.float64), want, f"decode by total keys B={B} d={d}")
+
+
+@pytest.mark.parametrize("name", ["b64_1k_8k", "b16_rag_like", "b8_skewed"])
+def test_decode_plan_by_total_keys(name):
+    """Ragged batches that take the plan by total keys (long sequences get more chunks
+    than short ones, merged through the workspace): every row against the oracle, the
+    result bit-identical on a second call and to the allocation-free entry point (which
+    makes the same plan)."""
+    Hq, Hkv, d = 32, 8, 128
+    rng = np.random.Generator(np.random.PCG64(41))
+    if name == "b64_1k_8k":
+        ctx = [int(x) for x in rng.integers(1024, 8193, 64)]
+    elif name == "b16_rag_like":
+        ctx = [int(x) for x in rng.integers(1200, 4600, 16)]
+    else:   # one long sequence among short ones
+        ctx = [16000, 40, 300, 17, 1000, 2, 513, 64]
+    q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=43)
+    say(f"[gpu] decode plan by total keys {name}: B={len(ctx)} keys={sum(ctx)} max={max(ctx)} "
+        f"workspace={pcr.decode_attn_workspace_bytes(len(ctx), Hq, Hkv, d, max(ctx))}")
     out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
     got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
-    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode merged B={B} d={d}")
+    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode total-keys plan {name}")
+    again = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
+    assert torch.equal(out, again), "second call differs"
+    pool = pcr.KVPool(dev(pk), dev(pv), Hkv, d)
+    na = torch.zeros_like(out)
+    cl = np.asarray(ctx, np.int32)
+    pcr.decode_attn_noalloc(dev(q), pool, dev(bt), dev(cl), cl, Hq, na)
+    torch.cuda.synchronize()
+    assert torch.equal(out, na), "allocation-free entry point differs"
 
 
 NAN_BITS = np.uint16(0x7FC1)
@@ -127,11 +162,16 @@ def test_decode_nan_past_context_end(regime, B):
     q, pk, pv, bt = _decode_inputs(ctx, Hq, Hkv, d, seed=2000 + B)
     pk, pv = _poison_past_end(pk, pv, bt, ctx)
     ws = pcr.decode_attn_workspace_bytes(B, Hq, Hkv, d, max(ctx))
-    assert (ws > 0) == (regime == "workspace")
+    assert (ws > 0) == (regime != "one_chunk")
     say(f"[gpu] decode NaN past context end: {regime} B={B} max_ctx={max(ctx)} workspace={ws}")
-    out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d)
-    got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
-    _check(got, _decode_oracle(q, pk, pv, bt, ctx, Hkv), f"decode NaN tail {regime}")
+    want = _decode_oracle(q, pk, pv, bt, ctx, Hkv)
+    # lds_merge: a one-byte workspace keeps the plan by the largest context (chunks merged
+    # in the workgroup); the full workspace then takes the plan by total keys
+    runs = [torch.empty(1, dtype=torch.uint8, device="cuda"), None] if regime == "lds_merge" else [None]
+    for w in runs:
+        out = _decode_gpu(q, pk, pv, bt, ctx, Hq, Hkv, d, workspace=w)
+        got = synth.bf16_bits_to_f32(u16(out)).astype(np.float64)
+        _check(got, want, f"decode NaN tail {regime} ({'one-byte' if w is not None else 'queried'} workspace)")
 
 
 def test_decode_long_contexts():
