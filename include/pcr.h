@@ -324,9 +324,9 @@ pcr_status pcr_decode_attn(const void *q, const pcr_kv_pool *pool, const int32_t
  * back), so calls on one device that may overlap (different streams, or host
  * threads without ordering) race; order them on one stream.
  * Errors: as pcr_decode_attn, and PCR_ERR_UNSUPPORTED when the batch would need
- * more scratch than the maximum (pcr_decode_attn_workspace_size tells the size;
- * at most about 11 MiB for any batch on a 256-compute-unit GPU); the message
- * names both sizes.
+ * more scratch than the maximum (the plan by the largest context needs at most
+ * about 11 MiB for any batch on a 256-compute-unit GPU, and the plan by total keys
+ * is taken only when it fits); the message names both sizes.
  */
 #define PCR_DECODE_NOALLOC_SCRATCH_BYTES (16 << 20)
 pcr_status pcr_decode_attn_noalloc(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables,
