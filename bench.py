@@ -631,6 +631,55 @@ def measure_decode_ragged():
                            name="decode RAG mix 16 requests", prefill_beside=False)]
 
 
+def measure_mixed(n_dec=64, ctx=4352, steps=20, seed=81):
+    """A mixed batch through one prefill launch: the RAG mix's 16 prefill requests plus
+    n_dec decode rows (one new token over ctx keys each), against the prefill requests
+    alone and the decode rows alone through the same entry point. Pool and Q drawn on
+    the device (the values do not change the work)."""
+    import torch
+    from paper_2603_23049_amd import pcr, synth
+    rag = workload("rag_mix")
+    Hq, Hkv, d, bs = rag.num_q_heads, rag.num_kv_heads, rag.head_dim, rag.block_size
+    cases = {"prefill_only": (list(rag.prefix_lens), list(rag.suffix_lens)),
+             "decode_only": ([ctx - 1] * n_dec, [1] * n_dec),
+             "mixed": (list(rag.prefix_lens) + [ctx - 1] * n_dec, list(rag.suffix_lens) + [1] * n_dec)}
+    s = torch.cuda.current_stream()
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    rec = {"workload": f"RAG mix {len(rag.prefix_lens)} requests + {n_dec} decode rows of {ctx} keys, "
+                       f"Hq={Hq} Hkv={Hkv} d={d}, one prefill launch"}
+    for name, (pl_l, sl_l) in cases.items():
+        nb = sum(-(-(a + b) // bs) for a, b in zip(pl_l, sl_l))
+        b = synth.ragged_batch(name, Hq=Hq, Hkv=Hkv, d=d, prefix_lens=pl_l, suffix_lens=sl_l, pool_blocks=nb,
+                               seed=seed)
+        pk = torch.randn((nb, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+        pv = torch.randn((nb, Hkv, bs * d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+        pool = pcr.KVPool(pk, pv, Hkv, d)
+        q = torch.randn((b.T, Hq, d), device="cuda", dtype=torch.bfloat16, generator=g).view(torch.int16)
+        out = torch.empty_like(q)
+        pl_h = np.asarray(pl_l, np.int32)
+        cu_h = np.concatenate([[0], np.cumsum(sl_l)]).astype(np.int32)
+        bt = torch.from_numpy(np.ascontiguousarray(b.block_tables)).cuda()
+        pl, cu = torch.from_numpy(pl_h).cuda(), torch.from_numpy(cu_h).cuda()
+
+        def fn():
+            pcr.prefix_prefill_attn(q, pool, bt, pl, cu, pl_h, cu_h, Hq, out, stream=s)
+
+        warm_up(fn, 200.0)
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(steps):
+            fn()
+        e.record(s)
+        e.synchronize()
+        ms = a.elapsed_time(e) / steps
+        rec[f"{name}_ms"] = ms
+        rec[f"{name}_tflops"] = attention_flops(pl_l, sl_l, Hq, d) / ms / 1e9
+        del pk, pv, q, out, pool
+        torch.cuda.empty_cache()
+    rec["mixed_over_prefill_ms"] = rec["mixed_ms"] - rec["prefill_only_ms"]
+    return rec
+
+
 def measure_prefetch(windows=(0, 4, 6), chunk_mib=4, dram_sweep=(48, 96, 192), request_compute_ms=30.0,
                      n_serve=40):
     """Serving loop through DRAM and SSD tiers with the queue-window prefetch: SSD stall
@@ -1068,7 +1117,8 @@ def _main(args, sampler):
         copy_calibration()
         return 0
     if args.decode_only:
-        print(json.dumps({"decode": measure_decode(), "decode_ragged": measure_decode_ragged()}), flush=True)
+        print(json.dumps({"decode": measure_decode(), "decode_ragged": measure_decode_ragged(),
+                          "mixed": measure_mixed()}), flush=True)
         return 0
     if args.append_sweep_only:
         print(json.dumps({"append_sweep": measure_append_sweep()}), flush=True)
@@ -1195,6 +1245,8 @@ def _main(args, sampler):
         _say("[bench] decode step")
         extra["decode"] = measure_decode()
         extra["decode_ragged"] = measure_decode_ragged()
+        _say("[bench] mixed prefill + decode launch")
+        extra["mixed"] = measure_mixed()
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
         rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=200.0)
@@ -1266,7 +1318,8 @@ def _main(args, sampler):
         "wall_ms_per_step": st["wall_ms_per_step"],
         "graph_ms_per_step": st["graph_step_ms"],
     }
-    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "decode_ragged", "prefetch",
+    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "decode_ragged", "mixed",
+                                          "prefetch",
                                           "append_sweep", "hit_ratio")})
     print(json.dumps(rec), flush=True)
     return 0

@@ -236,6 +236,10 @@ pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void 
  * element the error is about 2^-8 max_j |v_j - out| plus half a bf16 ulp of out.
  * Every key position j <= p_b + s_b - 1 must hold valid data (loaded or appended);
  * slots past p_b + s_b are never read into the result.
+ * Mixed batches: a sequence with s_b = 1 (a decode row) and Hq / Hkv <= 16 is
+ * computed in the same launch by a decode workgroup (the key range split over its
+ * waves, the same numerics as pcr_decode_attn), and such rows are spread over the
+ * prefill row tiles of the launch so that they run beside them.
  */
 pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
                                    const int32_t *block_tables, int32_t max_blocks,

@@ -49,6 +49,7 @@
 #include <atomic>
 #include <type_traits>
 
+#include "decode_wave.h"
 #include "pcr_internal.h"
 
 namespace pcr {
@@ -140,7 +141,17 @@ __device__ __forceinline__ void phase_barrier()
 __device__ __forceinline__ void dma16(const char *base, uint32_t lane_off, uint32_t lds_dst)
 {
     const unsigned m0 = __builtin_amdgcn_readfirstlane(lds_dst);
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(base), "s"(m0)
+    // The base is wave-uniform; reading it through readfirstlane states that to the
+    // register allocator (free when it already sits in SGPRs), which otherwise may keep
+    // it in VGPRs under SGPR pressure and then cannot meet the "s" constraint.
+    // (readfirstlane returns int: each half goes through uint32_t before widening, or a
+    // low word with bit 31 set would sign-extend into the high half of the address)
+    const uint64_t b64 = reinterpret_cast<uint64_t>(base);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b64 >> 32));
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b64);
+    const uint64_t sb = (hi << 32) | lo;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off),
+                 "s"(reinterpret_cast<const char *>(sb)), "s"(m0)
                  : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -171,6 +182,85 @@ struct AttnWorkMap {
     int32_t first[kMaxMapSeqs];         // the slot's first new token (row of q and out)
     int32_t count[kMaxMapSeqs];         // the slot's new tokens s
 };
+
+// A sequence with one new token in a prefill launch (a decode row, Sec. 2.2; prefill
+// and decode rows in one pass, Sec. 4.3): its G rows would fill G columns of the
+// 128- or 256-row tiles, and the workgroup would spend the matrix time of the whole
+// tile on them while its loads sit idle. Its workgroup instead runs the decode
+// kernel's wave routine (decode_wave.h): the 8 waves each take one chunk of the keys
+// (with two register sets, which the prefill kernel's register budget allows) and
+// merge their (O, max, sum) through LDS. The work is then bound by reading K/V, and
+// it overlaps the matrix-bound workgroups of the prefill rows on the other compute
+// units.
+template <int D>
+__device__ __forceinline__ void decode_workgroup(const u16 *__restrict__ q, const u16 *__restrict__ pool_k,
+                                                 const u16 *__restrict__ pool_v, int32_t num_blocks, int32_t Hkv,
+                                                 const int32_t *__restrict__ bt_row, int32_t max_blocks, int g, int G,
+                                                 int32_t Hq, int p, int64_t t0, float scale_log2,
+                                                 u16 *__restrict__ out, char *lds)
+{
+    constexpr int MT = D / 16;
+    constexpr int kWaves = kThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n_keys = p + 1;                       // keys 0 .. p: the row's causal range
+    const int chunk = ((n_keys + kWaves - 1) / kWaves + decode_wave::kStepKeys - 1) / decode_wave::kStepKeys *
+                      decode_wave::kStepKeys;
+    const int kbeg = wave * chunk;
+    const int kend = min(n_keys, kbeg + chunk);
+    const int last_blk = max(0, min((n_keys - 1) >> 4, max_blocks - 1));
+    const int c = lane & 15, q4 = lane >> 4;
+    const bool col = c < G;
+    const int h = g * G + c;
+    f32x4 o[MT];
+    float m_run = -INFINITY, l_run = 0.f;
+    if (kbeg < n_keys) {
+        const u16 *qrow = q + (t0 * Hq + (col ? h : g * G)) * D + 8 * q4;
+        decode_wave::chunk<D, 2>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, bt_row, last_blk, kbeg, kend,
+                                 scale_log2, o, m_run, l_run);
+    } else {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    // Waves 1.. leave O (lane layout), max and sum in LDS; wave 0 merges and writes. A
+    // chunk past the end contributes max -inf, sum 0, O 0; chunk 0 always has keys.
+    f32x4 *part_o = reinterpret_cast<f32x4 *>(lds);                         // [wave][MT][64 lanes]
+    float *part_ml = reinterpret_cast<float *>(part_o + kWaves * MT * 64);   // [wave][64 lanes][2]
+    if (wave > 0) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) part_o[(wave * MT + mt) * 64 + lane] = o[mt];
+        part_ml[2 * (wave * 64 + lane)] = m_run;
+        part_ml[2 * (wave * 64 + lane) + 1] = l_tot;
+    }
+    __syncthreads();
+    // (no early return here: a return on a lane condition inside this inlined function
+    // made the compiler treat the prefill path's block offsets as divergent)
+    if (wave == 0) {
+        float M = m_run;
+        for (int w = 1; w < kWaves; ++w) M = fmaxf(M, part_ml[2 * (w * 64 + lane)]);
+        const float a0 = __builtin_amdgcn_exp2f(m_run - M);
+        l_tot *= a0;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) o[mt] *= a0;
+        for (int w = 1; w < kWaves; ++w) {
+            const float a = __builtin_amdgcn_exp2f(part_ml[2 * (w * 64 + lane)] - M);
+            l_tot += a * part_ml[2 * (w * 64 + lane) + 1];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) o[mt] += a * part_o[(w * MT + mt) * 64 + lane];
+        }
+        if (col) {
+            const float inv = 1.f / l_tot;
+            u16 *orow = out + (t0 * Hq + h) * D + 4 * q4;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const bf16x4 v = __builtin_convertvector(o[mt] * inv, bf16x4);
+                *reinterpret_cast<u32x2 *>(orow + 16 * mt) = __builtin_bit_cast(u32x2, v);
+            }
+        }
+    }
+}
 
 template <int D, bool ROWS>
 __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
@@ -259,6 +349,13 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int rows_total = s * G;
     const int row0 = rt * RPW;
     if (s <= 0 || row0 >= rows_total || T <= 0) return;   // uniform over the workgroup
+    if (s == 1 && G <= decode_wave::kMaxCols) {           // a decode row (uniform too)
+        static_assert(kThreads / 64 * (D / 16) * 64 * 16 + kThreads / 64 * 64 * 8 <= (int)sizeof(lds), "merge area");
+        if (t0 < T)
+            decode_workgroup<D>(q, pool_k, pool_v, num_blocks, Hkv, block_tables + (int64_t)b * max_blocks,
+                                max_blocks, g, G, Hq, p, t0, scale_log2, out, &lds[0][0]);
+        return;
+    }
     const int total = p + s;
 
     // This lane's packed query row (rows past the end compute a copy of the last row).
@@ -333,12 +430,12 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
 
     const int32_t *bt = block_tables + (int64_t)b * max_blocks;
     const int lgrp = ROWS ? 0 : grp;        // whose tile buffers this group reads
-    auto kbuf = [&](int j) { return &lds[lgrp][(j & 1) * Geo::KBYTES]; };
-    auto vbuf = [&](int j) { return &lds[lgrp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
+    auto kbuf = [&](int j) __attribute__((always_inline)) { return &lds[lgrp][(j & 1) * Geo::KBYTES]; };
+    auto vbuf = [&](int j) __attribute__((always_inline)) { return &lds[lgrp][2 * Geo::KBYTES + (j & 1) * Geo::VBYTES]; };
     // The same buffers as LDS byte addresses, for the direct loads (no generic-pointer casts).
     const uint32_t lds_addr = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)&lds[lgrp][0];
-    auto kbuf_off = [&](int j) { return (uint32_t)((j & 1) * Geo::KBYTES); };
-    auto vbuf_off = [&](int j) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
+    auto kbuf_off = [&](int j) __attribute__((always_inline)) { return (uint32_t)((j & 1) * Geo::KBYTES); };
+    auto vbuf_off = [&](int j) __attribute__((always_inline)) { return (uint32_t)(2 * Geo::KBYTES + (j & 1) * Geo::VBYTES); };
 
     // Pool block ids of this group's tile j, read raw (as scalars) one phase before
     // use. Logical blocks past the sequence read the last valid entry, so the four loads
@@ -347,7 +444,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // the last tile, so any in-pool block can stand in there; an id outside the pool
     // becomes block 0, so no load ever leaves the pool.
     const char *bt_bytes = reinterpret_cast<const char *>(bt);
-    auto tile_ids = [&](int j, int32_t (&ids)[kTileBlocks]) {
+    auto tile_ids = [&](int j, int32_t (&ids)[kTileBlocks]) __attribute__((always_inline)) {
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) {
             const uint32_t lb = (uint32_t)min((tile_begin + j) * kTileBlocks + jb, valid_blocks - 1);
@@ -357,11 +454,11 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // Byte offset of the (pool block, kv head g) payload of a raw block id; an id outside
     // the pool becomes block 0. (blk * Hkv + g fits in 32 bits for any pool that fits in
     // memory: 2^32 payloads would be 8 TB.)
-    auto payload_off = [&](int32_t blk) -> int64_t {
+    auto payload_off = [&](int32_t blk) __attribute__((always_inline)) -> int64_t {
         const uint32_t b = (uint32_t)blk < (uint32_t)num_blocks ? (uint32_t)blk : 0u;
         return (int64_t)(b * (uint32_t)Hkv + (uint32_t)g) * kPayloadBytes;
     };
-    auto to_offs = [&](const int32_t (&ids)[kTileBlocks], int64_t (&offs)[kTileBlocks]) {
+    auto to_offs = [&](const int32_t (&ids)[kTileBlocks], int64_t (&offs)[kTileBlocks]) __attribute__((always_inline)) {
 #pragma unroll
         for (int jb = 0; jb < kTileBlocks; ++jb) offs[jb] = payload_off(ids[jb]);
     };
@@ -385,15 +482,15 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // wave-wide load; the LDS swizzle is applied through each lane's source.
     // One direct load (load u of the tile's K or V) of this group's tile j into its buffer:
     // a 1 KB slab per wave-wide load; the LDS swizzle is applied through each lane's source.
-    auto load_k = [&](int j, const int64_t (&offs)[kTileBlocks], int u) {
+    auto load_k = [&](int j, const int64_t (&offs)[kTileBlocks], int u) __attribute__((always_inline)) {
         const int slab = u * kGroupWaves + wg;                             // wave-uniform
         dma16(pool_k_bytes + offs[slab / kSlabs], k_off, lds_addr + kbuf_off(j) + slab * 1024);
     };
-    auto load_v = [&](int j, const int64_t (&offs)[kTileBlocks], int u) {
+    auto load_v = [&](int j, const int64_t (&offs)[kTileBlocks], int u) __attribute__((always_inline)) {
         const int slab = u * kGroupWaves + wg;
         dma16(pool_v_bytes + offs[slab / kSlabs], v_off, lds_addr + vbuf_off(j) + slab * 1024);
     };
-    auto issue_k = [&](int j, const int64_t (&offs)[kTileBlocks]) {
+    auto issue_k = [&](int j, const int64_t (&offs)[kTileBlocks]) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < kKLoads; ++u) load_k(j, offs, u);
     };
@@ -401,7 +498,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // ---- matrix work: O^T += V^T(j) P^T(j), k-step t = pool block t of the tile.
     // In the tile holding the sequence end, V entries of keys >= total are cleared
     // in the operand (their slots may hold anything; 0 * NaN would poison O).
-    auto pv = [&](int j, const bf16x8 (&pf)[kTileBlocks], auto clear_tag) {
+    auto pv = [&](int j, const bf16x8 (&pf)[kTileBlocks], auto clear_tag) __attribute__((always_inline)) {
         constexpr bool CLEAR = decltype(clear_tag)::value;
         const char *tv = vbuf(j);
         const int vlim = total - (tile_begin + j) * kTileKeys;     // valid keys in the tile
@@ -432,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     // V(j+1) and K(j+2), one per few MFMAs, so the texture path never backs up a wave.
     auto matrix_cluster = [&](auto pv_tag, auto qk_tag, int j, const bf16x8 (&pf)[kTileBlocks],
                               f32x16 (&st)[2], int64_t (&idv)[kTileBlocks], int64_t (&idk)[kTileBlocks],
-                              auto convert_tag, auto load_tag) {
+                              auto convert_tag, auto load_tag) __attribute__((always_inline)) {
         constexpr bool DO_PV = decltype(pv_tag)::value, DO_QK = decltype(qk_tag)::value;
         constexpr bool LOADS = decltype(load_tag)::value;
 
@@ -443,7 +540,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
         constexpr int kAhead = KAHEAD;
         const char *tv = vbuf(j);
         const char *tk = kbuf(j + 1);
-        auto frag = [&](int i) -> u32x4 {
+        auto frag = [&](int i) __attribute__((always_inline)) -> u32x4 {
             if (i < NPV) {
                 const int t = i / MT, mt = i % MT;
                 const int d = 32 * mt + qc;
@@ -508,7 +605,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     };
 
     // ---- vector work: online softmax of S^T(j) into bf16 P(j) (lazy rescale) ----
-    auto softmax = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) {
+    auto softmax = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks]) __attribute__((always_inline)) {
         l_run += (lane & 16) ? tsum[1] : tsum[0];   // tile j-1 (zero before the first tile)
         const int kbase = (tile_begin + j) * kTileKeys;
         if (kbase + kTileKeys - 1 > w_min_limit) {
@@ -611,14 +708,14 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const int n0 = split, n1 = ROWS ? ntiles : ntiles - split;
     const int phases = max(2 * n0 + 1, 2 * n1 + 2);
     int ph = 0;
-    auto phase_end = [&]() {
+    auto phase_end = [&]() __attribute__((always_inline)) {
         phase_barrier();
         ++ph;
     };
     // M(j): softmax of tile j; block ids of tile j+2 (read now, range-checked and
     // converted at the start of C(j)) when this group loads; then wait for the loads
     // C(j-1) issued.
-    auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks], auto load_tag) {
+    auto vector_cluster = [&](int j, f32x16 (&st)[2], bf16x8 (&pf)[kTileBlocks], auto load_tag) __attribute__((always_inline)) {
         // The scalar loads of the ids go out before the softmax, whose length covers
         // their latency (left to itself the scheduler sinks them next to their use).
         if constexpr (decltype(load_tag)::value) tile_ids(j + 2, ids_raw);
@@ -636,7 +733,7 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     if (grp == 1) phase_end();
     // The tile loop, instantiated once for a group that loads and once for one that
     // only reads (row halves, group 1), so that no branch splits a matrix cluster.
-    auto run_tiles = [&](auto load_tag) {
+    auto run_tiles = [&](auto load_tag) __attribute__((always_inline)) {
         constexpr std::true_type T_{};
         constexpr std::false_type F_{};
         // C(-1): QK(0), loads of V(0) and K(1) (K(1) lands in an unused buffer if n == 1)
@@ -817,7 +914,34 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
         rows = sched == PCR_ATTN_SCHEDULE_ROW_HALVES ||
                (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)n_cu);
         const int64_t rpw = rows ? 2 * kRowsPerWG : kRowsPerWG;
+        // Longest contexts first. Decode rows (one new token, one workgroup each, bound by
+        // HBM) are then spread evenly over the prefill tiles (bound by the matrix cores):
+        // run back to back they would take every compute unit at once and queue on HBM.
         std::stable_sort(wm.seq, wm.seq + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
+        {
+            const bool dec_rows = G <= decode_wave::kMaxCols;
+            int32_t pre[kMaxMapSeqs], dec[kMaxMapSeqs];
+            int np = 0, nd = 0;
+            int64_t pre_tiles = 0;
+            for (int k = 0; k < n; ++k) {
+                const int b = wm.seq[k];
+                if (dec_rows && rows_of[b] == G) {
+                    dec[nd++] = b;
+                } else {
+                    pre[np++] = b;
+                    pre_tiles += (rows_of[b] + rpw - 1) / rpw;
+                }
+            }
+            if (nd > 0 && np > 0) {
+                int m = 0, di = 0;
+                int64_t done = 0;
+                for (int k = 0; k < np; ++k) {
+                    wm.seq[m++] = pre[k];
+                    done += (rows_of[pre[k]] + rpw - 1) / rpw;
+                    for (; di < nd && (int64_t)di * pre_tiles < (int64_t)nd * done; ++di) wm.seq[m++] = dec[di];
+                }
+            }
+        }
         int32_t cum = 0;
         for (int k = 0; k < n; ++k) {
             const int b = wm.seq[k];

@@ -11,23 +11,12 @@
 //
 // Work decomposition. The key range of each (sequence, kv head) is cut into
 // n_split chunks of `chunk` keys (a multiple of 32). Each chunk is the work of
-// one wave; the host picks n_split so that every SIMD gets about one wave. A
-// wave holds the G query heads of its kv head as the columns of
-// v_mfma_f32_16x16x32_bf16 tiles (G <= 16) and walks its chunk 32 keys (two
-// pool blocks) at a time:
-//   S^T[key][h] = K Q^T     A = 16 key rows x 32 dims of K,  B = Q^T (registers)
-//   O^T[d][h]  += V^T P^T   A = 16 dims x 32 keys of V^T,    B = P^T (registers)
-// No operand is shared between waves, so K and V go from HBM straight into
-// registers: K is key-major and V d-major inside each pool block, so every A
-// operand is one 16-byte run. Three register sets rotate: the loads of the next
-// 64 keys are in flight while the current 32 are used. Lane (c, q4)
-// (c = lane % 16, q4 = lane / 16) loads key row 8*(c/4) + 4r + c%4 for the r-th
-// K product, so that its eight scores are keys 8*q4 .. 8*q4 + 7 of the step,
-// which are exactly its eight P^T operand values in the V product: the
-// softmax is in-lane apart from the column max over the four lanes of a column.
-//
-// K/V loads are non-temporal: every byte is used once, and streaming them past
-// the caches measured about 10% faster than ordinary loads.
+// one wave (decode_wave::chunk, decode_wave.h: the G query heads as MFMA columns,
+// K and V straight from HBM into registers, here with three register sets so that
+// two steps of loads are in flight while a third is used); the host picks n_split
+// so that every SIMD gets about one wave. The loads are non-temporal: every byte
+// is used once, and streaming them past the caches measured about 10% faster than
+// ordinary loads.
 //
 // A chunk that covers its whole sequence writes the output row. Up to four
 // chunks of one (sequence, kv head) form one workgroup and are merged through
@@ -37,6 +26,7 @@
 #include <algorithm>
 #include <mutex>
 
+#include "decode_wave.h"
 #include "pcr_internal.h"
 
 // Scratch of the allocation-free decode entry point: the split kernel's partial
@@ -59,22 +49,14 @@ typedef unsigned short u16;
 
 constexpr int kWaves = 4;              // tasks (waves) per workgroup
 constexpr int kThreads = 64 * kWaves;
-constexpr int kStepKeys = 32;          // keys per step: two pool blocks
-constexpr int kMaxCols = 16;           // query heads per kv head held by one tile
+constexpr int kStepKeys = decode_wave::kStepKeys;   // keys per step: two pool blocks
+constexpr int kMaxCols = decode_wave::kMaxCols;   // query heads per kv head held by one tile
 // Waves per CU the split count aims at: one per SIMD, each with three register sets
 // of K/V loads (two steps in flight while a third is used), measured faster than
 // two waves per SIMD with two sets each.
 constexpr int waves_per_cu(int) { return 4; }
 constexpr int kMinChunk = 256;         // keys; shorter chunks spend more on set-up than on loads
 constexpr float kLog2e = 1.4426950408889634f;
-
-__device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-template <int D>
-struct StepRegs {
-    u32x4 k[2][D / 32];   // K operands of the two products (row group r, dims 32*kk ..)
-    u32x4 v[D / 16];      // V^T operands (dims 16*mt ..)
-};
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) void decode_split_kernel(
@@ -84,7 +66,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
     float scale_log2, int32_t lds_merge, u16 *__restrict__ out, float *__restrict__ ws_o,
     float *__restrict__ ws_ml)
 {
-    constexpr int KK = D / 32;    // K products per row group (32 dims each)
     constexpr int MT = D / 16;    // V products (16 dims each)
     const int lane = (int)(threadIdx.x & 63);
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -105,139 +86,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
     const bool col = c < G;
     const int h = g * G + c;
 
-    // Q^T operands: lane (c, q4) holds dims 32*kk + 8*q4 .. +7 of head h (zero past G).
-    u32x4 qf[KK];
-    {
-        const u16 *qrow = q + ((int64_t)b * Hq + (col ? h : g * G)) * D + 8 * q4;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            const u32x4 raw = *reinterpret_cast<const u32x4 *>(qrow + 32 * kk);
-            qf[kk] = col ? raw : u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-
-    const int32_t *bt_row = block_tables + (int64_t)b * max_blocks;
-    auto block_id = [&](int li) -> int32_t {
-        const int32_t id = bt_row[min(li, last_blk)];
-        return (uint32_t)id < (uint32_t)num_blocks ? id : 0;   // a bad entry reads block 0, never outside
-    };
-    const int krow = 8 * ((c >> 2) & 1) + (c & 3);    // slot of row group 0; row group 1 is 4 slots on
-    auto load_step = [&](int step, StepRegs<D> &R) {
-        const int li = (kbeg + step * kStepKeys) >> 4;
-        const int32_t b0 = block_id(li), b1 = block_id(li + 1);
-        const int32_t kb = (c >> 3) ? b1 : b0;
-        const int32_t vb = (q4 >> 1) ? b1 : b0;
-        const u16 *kp = pool_k + ((int64_t)kb * Hkv + g) * (kBlockSize * D) + krow * D + 8 * q4;
-        const u16 *vp = pool_v + ((int64_t)vb * Hkv + g) * (kBlockSize * D) + c * kBlockSize + 8 * (q4 & 1);
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk)
-                R.k[r][kk] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(kp + 4 * r * D + 32 * kk));
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            R.v[mt] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(vp + 16 * mt * kBlockSize));
-    };
-
-    float m_run = -INFINITY, l_run = 0.f;
     f32x4 o[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto process = [&](int step, const StepRegs<D> &R) {
-        f32x4 s[2];
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            s[r] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk)
-                s[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(R.k[r][kk]), as_bf16x8(qf[kk]), s[r],
-                                                               0, 0, 0);
-        }
-        const int k0 = kbeg + step * kStepKeys;
-        const bool ragged = k0 + kStepKeys > kend;  // wave-uniform: only a chunk's last step is ragged
-        if (ragged) {
-#pragma unroll
-            for (int r = 0; r < 2; ++r)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (k0 + 8 * q4 + 4 * r + i >= kend) s[r][i] = -INFINITY;
-        }
-        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * scale_log2);   // finite: key k0 is visible
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        bf16x8 pb;
-        float ps = 0.f;
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r][i], scale_log2, -m_new));
-                pb[4 * r + i] = (__bf16)p;
-                ps += (float)pb[4 * r + i];     // the rounded value the product weights V with
-            }
-        l_run = l_run * alpha + ps;
-        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {   // the max rose in some column
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
-        }
-        // In a ragged step the V^T operand entries of keys >= kend are cleared: their P is 0,
-        // but the slots past a context's end may hold anything (never written, or another
-        // request's data), and 0 * NaN or 0 * Inf would poison every output column. The
-        // lane's 8 values are keys k0 + 8*q4 .. +7, the same keys as its P^T operand.
-        const int nvalid = kend - (k0 + 8 * q4);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            u32x4 vv = R.v[mt];
-            if (ragged) {
-#pragma unroll
-                for (int wd = 0; wd < 4; ++wd)
-                    vv[wd] &= (2 * wd < nvalid ? 0x0000FFFFu : 0u) | (2 * wd + 1 < nvalid ? 0xFFFF0000u : 0u);
-            }
-            o[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pb, o[mt], 0, 0, 0);
-        }
-    };
-
+    float m_run = -INFINITY, l_run = 0.f;
     if (active) {
-        // Three register sets rotate. Every load inside the loop is unconditional (the
-        // second prologue load rereads step 0 for a one-step chunk), so the wait before
-        // each step leaves the two later steps' loads in flight.
-        const int n_steps = (kend - kbeg + kStepKeys - 1) / kStepKeys;
-        StepRegs<D> ra, rb, rc;
-        load_step(0, ra);
-        load_step(min(1, n_steps - 1), rb);
-        int j = 0;
-        for (; j + 4 < n_steps; j += 3) {
-            load_step(j + 2, rc);
-            process(j, ra);
-            load_step(j + 3, ra);
-            process(j + 1, rb);
-            load_step(j + 4, rb);
-            process(j + 2, rc);
-        }
-        const int left = n_steps - j;               // 1 .. 4; ra holds step j, rb step j + 1
-        if (left == 1) {
-            process(j, ra);
-        } else if (left == 2) {
-            process(j, ra);
-            process(j + 1, rb);
-        } else if (left == 3) {
-            load_step(j + 2, rc);
-            process(j, ra);
-            process(j + 1, rb);
-            process(j + 2, rc);
-        } else {
-            load_step(j + 2, rc);
-            process(j, ra);
-            load_step(j + 3, ra);
-            process(j + 1, rb);
-            process(j + 2, rc);
-            process(j + 3, ra);
-        }
+        const u16 *qrow = q + ((int64_t)b * Hq + (col ? h : g * G)) * D + 8 * q4;
+        decode_wave::chunk<D, 3>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, block_tables + (int64_t)b * max_blocks,
+                                 last_blk, kbeg, kend, scale_log2, o, m_run, l_run);
+    } else {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
     float l_tot = l_run + __shfl_xor(l_run, 16);
