@@ -632,10 +632,11 @@ def measure_decode_ragged():
 
 
 def measure_mixed(n_dec=64, ctx=4352, steps=20, seed=81):
-    """A mixed batch through one prefill launch: the RAG mix's 16 prefill requests plus
-    n_dec decode rows (one new token over ctx keys each), against the prefill requests
-    alone and the decode rows alone through the same entry point. Pool and Q drawn on
-    the device (the values do not change the work)."""
+    """A mixed batch through the prefill entry point: the RAG mix's 16 prefill requests
+    plus n_dec decode rows (one new token over ctx keys each), against the prefill
+    requests alone and the decode rows alone through the same entry point (one launch
+    up to 128 sequences, consecutive launches beyond). Pool and Q drawn on the device
+    (the values do not change the work)."""
     import torch
     from paper_2603_23049_amd import pcr, synth
     rag = workload("rag_mix")
@@ -646,7 +647,7 @@ def measure_mixed(n_dec=64, ctx=4352, steps=20, seed=81):
     s = torch.cuda.current_stream()
     g = torch.Generator(device="cuda").manual_seed(seed)
     rec = {"workload": f"RAG mix {len(rag.prefix_lens)} requests + {n_dec} decode rows of {ctx} keys, "
-                       f"Hq={Hq} Hkv={Hkv} d={d}, one prefill launch"}
+                       f"Hq={Hq} Hkv={Hkv} d={d}, prefill entry point"}
     for name, (pl_l, sl_l) in cases.items():
         nb = sum(-(-(a + b) // bs) for a, b in zip(pl_l, sl_l))
         b = synth.ragged_batch(name, Hq=Hq, Hkv=Hkv, d=d, prefix_lens=pl_l, suffix_lens=sl_l, pool_blocks=nb,
@@ -1118,7 +1119,7 @@ def _main(args, sampler):
         return 0
     if args.decode_only:
         print(json.dumps({"decode": measure_decode(), "decode_ragged": measure_decode_ragged(),
-                          "mixed": measure_mixed()}), flush=True)
+                          "mixed": measure_mixed(), "mixed_256": measure_mixed(n_dec=256)}), flush=True)
         return 0
     if args.append_sweep_only:
         print(json.dumps({"append_sweep": measure_append_sweep()}), flush=True)
@@ -1245,8 +1246,9 @@ def _main(args, sampler):
         _say("[bench] decode step")
         extra["decode"] = measure_decode()
         extra["decode_ragged"] = measure_decode_ragged()
-        _say("[bench] mixed prefill + decode launch")
+        _say("[bench] mixed prefill + decode launches")
         extra["mixed"] = measure_mixed()
+        extra["mixed_256"] = measure_mixed(n_dec=256)
         rb = workload("rag_mix")
         _say(f"[bench] rag_mix attention (T={rb.T})")
         rst = measure_step(rb, max(10, args.steps // 4), 3, min_warm_ms=200.0)
@@ -1318,7 +1320,7 @@ def _main(args, sampler):
         "wall_ms_per_step": st["wall_ms_per_step"],
         "graph_ms_per_step": st["graph_step_ms"],
     }
-    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "decode_ragged", "mixed",
+    rec.update({k: extra.get(k) for k in ("l8b_layer", "rag_mix", "tp8_shard", "offload", "decode", "decode_ragged", "mixed", "mixed_256",
                                           "prefetch",
                                           "append_sweep", "hit_ratio")})
     print(json.dumps(rec), flush=True)

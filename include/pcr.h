@@ -263,7 +263,9 @@ pcr_status pcr_prefix_prefill_attn(const void *q, const pcr_kv_pool *pool,
  *     group on 128 of them over the whole key range, both reading one copy of
  *     each K/V tile (half the workgroups, each with one start-up and no merge for
  *     twice the work, and half the tile loads per row).
- * Batches of more than 128 sequences use key halves whatever the setting.
+ * A batch with more than 128 sequences with new tokens runs as consecutive launches
+ * on the stream, the sequences (longest context first) dealt round robin so that
+ * every launch gets the same mix; the schedule is chosen per launch.
  * Process-wide; takes effect at the next launch. PCR_ERR_INVALID_ARG for an
  * unknown value.
  */

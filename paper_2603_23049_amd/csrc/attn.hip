@@ -48,6 +48,7 @@
 #include <algorithm>
 #include <atomic>
 #include <type_traits>
+#include <vector>
 
 #include "decode_wave.h"
 #include "pcr_internal.h"
@@ -174,7 +175,7 @@ __device__ __forceinline__ void wait_vmem_keep()
 // the map (the kernel arguments) instead of a chain of dependent loads.
 constexpr int kMaxMapSeqs = 128;
 struct AttnWorkMap {
-    int32_t n_seq;                      // sequences with rows; 0: plain (b, g, rt) order
+    int32_t n_seq;                      // slots in use (sequences with new tokens)
     int32_t per_head;                   // row tiles of all sequences, one kv head
     int32_t seq[kMaxMapSeqs];           // sequence in each slot
     int32_t tiles_end[kMaxMapSeqs];     // row tiles of the slots up to and including this one
@@ -265,10 +266,8 @@ __device__ __forceinline__ void decode_workgroup(const u16 *__restrict__ q, cons
 template <int D, bool ROWS>
 __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
-    int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
-    const int32_t *__restrict__ prefix_lens, const int32_t *__restrict__ cu_suffix, int32_t Hq,
-    int32_t T, int32_t B, int32_t row_tiles, float scale_log2, float rescale_thr, u16 *__restrict__ out,
-    const AttnWorkMap wm)
+    int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks, int32_t Hq,
+    int32_t T, float scale_log2, float rescale_thr, u16 *__restrict__ out, const AttnWorkMap wm)
 {
     using Geo = TileGeom<D>;
     constexpr int CPR = Geo::CPR;
@@ -294,51 +293,39 @@ __global__ __launch_bounds__(kThreads) void prefill_attn_kernel(
     {
         const int x = (int)(blockIdx.x % kXcds), i = (int)(blockIdx.x / kXcds);
         const int per_xcd = (int)(gridDim.x / kXcds);
-        if (wm.n_seq > 0) {
-            int j;
-            if (Hkv % kXcds == 0) {
-                const int hh = i / wm.per_head;
-                g = x + kXcds * hh;
-                j = i - hh * wm.per_head;
-            } else {
-                const int w = x * per_xcd + i;
-                g = w / wm.per_head;
-                j = w - g * wm.per_head;
-            }
-            if (g >= Hkv) return;
-            // Slot of row tile j: the number of slots whose tiles end at or before j. Lane l
-            // reads slots l and l + 64 (all fields at once); the slot's fields are then taken
-            // from the lane that holds them.
-            int e[2], fs[2], fp[2], ft[2], fc[2];
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                const int k = lane + 64 * hf;
-                const bool in = k < wm.n_seq;
-                e[hf] = in ? wm.tiles_end[k] : INT32_MAX;
-                fs[hf] = in ? wm.seq[k] : 0;
-                fp[hf] = in ? wm.prefix[k] : 0;
-                ft[hf] = in ? wm.first[k] : 0;
-                fc[hf] = in ? wm.count[k] : 0;
-            }
-            const int slot = __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[0] <= j)) +
-                             __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[1] <= j));
-            const int hf = slot >> 6, sl = slot & 63;
-            b = __builtin_amdgcn_readlane(hf ? fs[1] : fs[0], sl);
-            p = __builtin_amdgcn_readlane(hf ? fp[1] : fp[0], sl);
-            t0 = __builtin_amdgcn_readlane(hf ? ft[1] : ft[0], sl);
-            s = __builtin_amdgcn_readlane(hf ? fc[1] : fc[0], sl);
-            rt = __builtin_amdgcn_readlane(hf ? e[1] : e[0], sl) - 1 - j;
+        int j;
+        if (Hkv % kXcds == 0) {
+            const int hh = i / wm.per_head;
+            g = x + kXcds * hh;
+            j = i - hh * wm.per_head;
         } else {
-            const int n_work = row_tiles * Hkv * B;
             const int w = x * per_xcd + i;
-            if (w >= n_work) return;
-            rt = w % row_tiles;
-            g = (w / row_tiles) % Hkv;
-            b = w / (row_tiles * Hkv);
-            p = prefix_lens[b];
-            t0 = cu_suffix[b];
-            s = cu_suffix[b + 1] - t0;
+            g = w / wm.per_head;
+            j = w - g * wm.per_head;
         }
+        if (g >= Hkv) return;
+        // Slot of row tile j: the number of slots whose tiles end at or before j. Lane l
+        // reads slots l and l + 64 (all fields at once); the slot's fields are then taken
+        // from the lane that holds them.
+        int e[2], fs[2], fp[2], ft[2], fc[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const int k = lane + 64 * hf;
+            const bool in = k < wm.n_seq;
+            e[hf] = in ? wm.tiles_end[k] : INT32_MAX;
+            fs[hf] = in ? wm.seq[k] : 0;
+            fp[hf] = in ? wm.prefix[k] : 0;
+            ft[hf] = in ? wm.first[k] : 0;
+            fc[hf] = in ? wm.count[k] : 0;
+        }
+        const int slot = __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[0] <= j)) +
+                         __builtin_popcountll(__builtin_amdgcn_ballot_w64(e[1] <= j));
+        const int hf = slot >> 6, sl = slot & 63;
+        b = __builtin_amdgcn_readlane(hf ? fs[1] : fs[0], sl);
+        p = __builtin_amdgcn_readlane(hf ? fp[1] : fp[0], sl);
+        t0 = __builtin_amdgcn_readlane(hf ? ft[1] : ft[0], sl);
+        s = __builtin_amdgcn_readlane(hf ? fc[1] : fc[0], sl);
+        rt = __builtin_amdgcn_readlane(hf ? e[1] : e[0], sl) - 1 - j;
     }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2;              // key halves: which half of the keys; row halves: of the rows
@@ -862,15 +849,97 @@ int attn_rows_per_workgroup(int) { return kRowsPerWG; }
 namespace {
 // Schedule override (pcr_prefill_attn_set_schedule): 0 chooses per launch.
 std::atomic<int> g_schedule{PCR_ATTN_SCHEDULE_AUTO};
+
 template <int D, bool ROWS>
 void launch_attn(dim3 grid, hipStream_t s, const u16 *qq, const u16 *pk, const u16 *pv, const pcr_kv_pool &pool,
-                 const int32_t *block_tables, int32_t max_blocks, const int32_t *prefix_lens,
-                 const int32_t *cu_suffix, int32_t num_q_heads, int32_t T, int32_t B, int32_t row_tiles,
-                 float scale_log2, float rescale_thr, u16 *oo, const AttnWorkMap &wm)
+                 const int32_t *block_tables, int32_t max_blocks, int32_t num_q_heads, int32_t T, float scale_log2,
+                 float rescale_thr, u16 *oo, const AttnWorkMap &wm)
 {
     hipLaunchKernelGGL((prefill_attn_kernel<D, ROWS>), grid, dim3(kThreads), 0, s, qq, pk, pv, pool.num_blocks,
-                       pool.num_kv_heads, block_tables, max_blocks, prefix_lens, cu_suffix, num_q_heads, T, B,
-                       row_tiles, scale_log2, rescale_thr, oo, wm);
+                       pool.num_kv_heads, block_tables, max_blocks, num_q_heads, T, scale_log2, rescale_thr, oo,
+                       wm);
+}
+
+// One launch over the sequences seq[0..n) (each with new tokens, n <= kMaxMapSeqs,
+// longest context first): builds the work map, picks the schedule, launches.
+hipError_t launch_group(const int32_t *seq, int n, const u16 *qq, const pcr_kv_pool &pool,
+                        const int32_t *block_tables, int32_t max_blocks, const int32_t *host_prefix_lens,
+                        const int32_t *host_cu_suffix, int32_t num_q_heads, int32_t T, float scale_log2,
+                        float rescale_thr, u16 *oo, hipStream_t s, int auto_schedule, int n_cu)
+{
+    const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv;
+    auto rows_of = [&](int32_t b) { return ((int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b]) * G; };
+    int64_t tiles_rows = 0;   // row tiles of 256 rows over the group's sequences, one kv head
+    for (int k = 0; k < n; ++k) tiles_rows += (rows_of(seq[k]) + 2 * kRowsPerWG - 1) / (2 * kRowsPerWG);
+    // Row halves when the launch keeps at least two workgroups per compute unit
+    // with them (each workgroup then pays its start-up and end for twice the work),
+    // unless the caller prefers key halves (shorter workgroups free a compute unit
+    // sooner for copy kernels that share the device).
+    int sched = g_schedule.load(std::memory_order_relaxed);
+    if (sched == PCR_ATTN_SCHEDULE_AUTO) sched = auto_schedule;
+    const bool rows = sched == PCR_ATTN_SCHEDULE_ROW_HALVES ||
+                      (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)n_cu);
+    const int64_t rpw = rows ? 2 * kRowsPerWG : kRowsPerWG;
+    auto tiles_of = [&](int32_t b) { return (rows_of(b) + rpw - 1) / rpw; };
+
+    // Slot order: the given order (longest context first), with the decode rows (one
+    // new token, one workgroup each, bound by HBM) spread evenly over the prefill
+    // tiles (bound by the matrix cores): run back to back they would take every
+    // compute unit at once and queue on HBM.
+    AttnWorkMap wm;
+    {
+        const bool dec_rows = G <= decode_wave::kMaxCols;
+        int32_t pre[kMaxMapSeqs], dec[kMaxMapSeqs];
+        int np = 0, nd = 0;
+        int64_t pre_tiles = 0;
+        for (int k = 0; k < n; ++k) {
+            if (dec_rows && rows_of(seq[k]) == G) {
+                dec[nd++] = seq[k];
+            } else {
+                pre[np++] = seq[k];
+                pre_tiles += tiles_of(seq[k]);
+            }
+        }
+        int m = 0, di = 0;
+        int64_t done = 0;
+        for (int k = 0; k < np; ++k) {
+            wm.seq[m++] = pre[k];
+            done += tiles_of(pre[k]);
+            for (; di < nd && (int64_t)di * pre_tiles < (int64_t)nd * done; ++di) wm.seq[m++] = dec[di];
+        }
+        for (; di < nd; ++di) wm.seq[m++] = dec[di];
+    }
+    int32_t cum = 0;
+    for (int k = 0; k < n; ++k) {
+        const int32_t b = wm.seq[k];
+        cum += (int32_t)tiles_of(b);
+        wm.tiles_end[k] = cum;
+        wm.prefix[k] = host_prefix_lens[b];
+        wm.first[k] = host_cu_suffix[b];
+        wm.count[k] = host_cu_suffix[b + 1] - host_cu_suffix[b];
+    }
+    wm.n_seq = n;
+    wm.per_head = cum;
+    const int64_t n_items = (Hkv % kXcds == 0) ? (int64_t)cum * Hkv : ((int64_t)cum * Hkv + kXcds - 1) / kXcds * kXcds;
+    const dim3 grid((unsigned)n_items);
+    auto *pk = static_cast<const u16 *>(pool.k);
+    auto *pv = static_cast<const u16 *>(pool.v);
+    if (pool.head_dim == 128) {
+        if (rows)
+            launch_attn<128, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, num_q_heads, T, scale_log2,
+                                   rescale_thr, oo, wm);
+        else
+            launch_attn<128, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, num_q_heads, T, scale_log2,
+                                    rescale_thr, oo, wm);
+    } else {
+        if (rows)
+            launch_attn<64, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, num_q_heads, T, scale_log2,
+                                  rescale_thr, oo, wm);
+        else
+            launch_attn<64, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, num_q_heads, T, scale_log2,
+                                   rescale_thr, oo, wm);
+    }
+    return hipGetLastError();
 }
 }  // namespace
 
@@ -884,103 +953,36 @@ hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       int32_t max_row_tiles, float sm_scale, void *out,
                                       hipStream_t s, int auto_schedule, int n_cu)
 {
-    const int Hkv = pool.num_kv_heads, G = num_q_heads / Hkv;
-    AttnWorkMap wm;
-    wm.n_seq = 0;
-    wm.per_head = 0;
-    int64_t n_items;
-    bool rows = false;
-    if (B <= kMaxMapSeqs) {
-        int32_t keys[kMaxMapSeqs];
-        int64_t rows_of[kMaxMapSeqs];
-        int n = 0;
-        int64_t tiles_rows = 0;   // row tiles of 256 rows over all sequences, one kv head
-        for (int b = 0; b < B; ++b) {
-            const int64_t sb = (int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b];
-            if (sb <= 0) continue;
-            wm.seq[n] = b;
-            rows_of[b] = sb * G;
-            keys[b] = (int32_t)(host_prefix_lens[b] + sb);
-            tiles_rows += (rows_of[b] + 2 * kRowsPerWG - 1) / (2 * kRowsPerWG);
-            ++n;
-        }
-        if (n == 0) return hipSuccess;
-        // Row halves when the launch keeps at least two workgroups per compute unit
-        // with them (each workgroup then pays its start-up and end for twice the work),
-        // unless the caller prefers key halves (shorter workgroups free a compute unit
-        // sooner for copy kernels that share the device).
-        int sched = g_schedule.load(std::memory_order_relaxed);
-        if (sched == PCR_ATTN_SCHEDULE_AUTO) sched = auto_schedule;
-        rows = sched == PCR_ATTN_SCHEDULE_ROW_HALVES ||
-               (sched == PCR_ATTN_SCHEDULE_AUTO && tiles_rows * Hkv >= 2 * (int64_t)n_cu);
-        const int64_t rpw = rows ? 2 * kRowsPerWG : kRowsPerWG;
-        // Longest contexts first. Decode rows (one new token, one workgroup each, bound by
-        // HBM) are then spread evenly over the prefill tiles (bound by the matrix cores):
-        // run back to back they would take every compute unit at once and queue on HBM.
-        std::stable_sort(wm.seq, wm.seq + n, [&](int32_t a, int32_t c) { return keys[a] > keys[c]; });
-        {
-            const bool dec_rows = G <= decode_wave::kMaxCols;
-            int32_t pre[kMaxMapSeqs], dec[kMaxMapSeqs];
-            int np = 0, nd = 0;
-            int64_t pre_tiles = 0;
-            for (int k = 0; k < n; ++k) {
-                const int b = wm.seq[k];
-                if (dec_rows && rows_of[b] == G) {
-                    dec[nd++] = b;
-                } else {
-                    pre[np++] = b;
-                    pre_tiles += (rows_of[b] + rpw - 1) / rpw;
-                }
-            }
-            if (nd > 0 && np > 0) {
-                int m = 0, di = 0;
-                int64_t done = 0;
-                for (int k = 0; k < np; ++k) {
-                    wm.seq[m++] = pre[k];
-                    done += (rows_of[pre[k]] + rpw - 1) / rpw;
-                    for (; di < nd && (int64_t)di * pre_tiles < (int64_t)nd * done; ++di) wm.seq[m++] = dec[di];
-                }
-            }
-        }
-        int32_t cum = 0;
-        for (int k = 0; k < n; ++k) {
-            const int b = wm.seq[k];
-            cum += (int32_t)((rows_of[b] + rpw - 1) / rpw);
-            wm.tiles_end[k] = cum;
-            wm.prefix[k] = host_prefix_lens[b];
-            wm.first[k] = host_cu_suffix[b];
-            wm.count[k] = host_cu_suffix[b + 1] - host_cu_suffix[b];
-        }
-        wm.n_seq = n;
-        wm.per_head = cum;
-        n_items = (Hkv % kXcds == 0) ? (int64_t)wm.per_head * Hkv
-                                     : ((int64_t)wm.per_head * Hkv + kXcds - 1) / kXcds * kXcds;
-    } else {
-        n_items = ((int64_t)max_row_tiles * Hkv * B + kXcds - 1) / kXcds * kXcds;
-    }
-    const dim3 grid((unsigned)n_items);
+    (void)prefix_lens;   // the lengths travel in the work map, from the host copies
+    (void)cu_suffix;
+    (void)max_row_tiles;
+    // The sequences with new tokens, longest context first.
+    std::vector<int32_t> seq;
+    seq.reserve((size_t)std::max(B, 0));
+    for (int32_t b = 0; b < B; ++b)
+        if (host_cu_suffix[b + 1] > host_cu_suffix[b]) seq.push_back(b);
+    if (seq.empty()) return hipSuccess;
+    auto keys = [&](int32_t b) { return (int64_t)host_prefix_lens[b] + host_cu_suffix[b + 1] - host_cu_suffix[b]; };
+    std::stable_sort(seq.begin(), seq.end(), [&](int32_t a, int32_t c) { return keys(a) > keys(c); });
     const float scale_log2 = sm_scale * kLog2e;
     const float rescale_thr = kRescaleThreshold / scale_log2;   // in units of <q,k>
     auto *qq = static_cast<const u16 *>(q);
-    auto *pk = static_cast<const u16 *>(pool.k);
-    auto *pv = static_cast<const u16 *>(pool.v);
     auto *oo = static_cast<u16 *>(out);
-    if (pool.head_dim == 128) {
-        if (rows)
-            launch_attn<128, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                   num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
-        else
-            launch_attn<128, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                    num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
-    } else {
-        if (rows)
-            launch_attn<64, true>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                  num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
-        else
-            launch_attn<64, false>(grid, s, qq, pk, pv, pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                   num_q_heads, T, B, max_row_tiles, scale_log2, rescale_thr, oo, wm);
+    // More sequences than one work map holds: consecutive launches on the stream, the
+    // sequences dealt round robin (sequence k of the sorted list to launch k mod
+    // n_launch), so that every launch gets the same mix of long and short ones.
+    const int n_act = (int)seq.size();
+    const int n_launch = (n_act + kMaxMapSeqs - 1) / kMaxMapSeqs;
+    int32_t group[kMaxMapSeqs];
+    for (int l = 0; l < n_launch; ++l) {
+        int n = 0;
+        for (int k = l; k < n_act; k += n_launch) group[n++] = seq[k];
+        const hipError_t e = launch_group(group, n, qq, pool, block_tables, max_blocks, host_prefix_lens,
+                                          host_cu_suffix, num_q_heads, T, scale_log2, rescale_thr, oo, s,
+                                          auto_schedule, n_cu);
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace pcr

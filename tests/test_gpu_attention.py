@@ -93,8 +93,9 @@ def test_edge_shapes(d, G):
 @pytest.mark.parametrize("B", [100, 140])
 def test_many_sequences(B):
     """More sequences than one lane of the work-map lookup holds (slots 64.. are read by
-    the second half of each lane's loads) and, at B = 140, more than the map holds
-    (plain order, lengths from the device arrays). Some sequences have no new tokens."""
+    the second half of each lane's loads) and, at B = 140, more than the map holds (133
+    with new tokens: two launches, the sequences dealt round robin). Some sequences have
+    no new tokens."""
     rng = np.random.Generator(np.random.PCG64(1000 + B))
     pl = [int(rng.integers(0, 80)) for _ in range(B)]
     sl = [int(rng.integers(0, 24)) for _ in range(B)]
@@ -108,6 +109,33 @@ def test_many_sequences(B):
     say(f"[gpu] attention many sequences B={b.B} T={b.T}")
     L = _run(b, data, pk0, pv0)
     _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"B={B}")
+
+
+@pytest.mark.parametrize("n_dec", [120, 280])
+def test_mixed_prefill_and_many_decode_rows(n_dec):
+    """Prefill requests among many decode rows (one new token each, contexts not a
+    multiple of 16): 8 + 120 sequences fill one work map, 8 + 280 take three launches
+    (sequences dealt round robin). Every row against the oracle, and the result
+    repeated bit for bit."""
+    rng = np.random.Generator(np.random.PCG64(3000 + n_dec))
+    pl = [int(rng.integers(100, 900)) for _ in range(8)] + [int(rng.integers(1, 700)) for _ in range(n_dec)]
+    sl = [int(rng.integers(60, 200)) for _ in range(8)] + [1] * n_dec
+    order = rng.permutation(len(pl))
+    pl, sl = [pl[i] for i in order], [sl[i] for i in order]
+    Hkv = 4
+    nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl)) + 3
+    b = synth.ragged_batch(f"mixed{n_dec}", Hq=4 * Hkv, Hkv=Hkv, d=128, prefix_lens=pl, suffix_lens=sl,
+                           pool_blocks=nblocks, seed=40 + n_dec)
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention mixed prefill + {n_dec} decode rows B={b.B} T={b.T}")
+    L = _run(b, data, pk0, pv0)
+    first = u16(L.out).copy()
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"mixed n_dec={n_dec}")
+    L.out.zero_()
+    L.attn()
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(L.out), first), "attention is not deterministic"
 
 
 def test_l8b_layer_full_and_deterministic():
