@@ -226,8 +226,10 @@ pcr_status pcr_append_kv(const pcr_kv_pool *pool, const void *k_new, const void 
  *   q              device bf16 [T][Hq][d]; T = cu_suffix[B]
  *   block_tables   device int32 [B][max_blocks]
  *   prefix_lens    device int32 [B];  cu_suffix device int32 [B+1]
- *   host_prefix_lens, host_cu_suffix   host copies of the same (used to size the launch;
- *                  they must equal the device arrays)
+ *   host_prefix_lens, host_cu_suffix   host copies of the same; they must equal the
+ *                  device arrays. The launch takes the lengths from these (they size it
+ *                  and travel in its arguments); the device arrays must be valid
+ *                  (non-NULL) but are not read.
  *   out            device bf16 [T][Hq][d]; fp32 accumulation, rounded to nearest even
  *   sm_scale       finite and > 0 (else PCR_ERR_INVALID_ARG)
  * Numerics: scores <q, k_j> and their scaling are fp32; the probabilities enter the

@@ -947,15 +947,10 @@ void attn_set_schedule(int schedule) { g_schedule.store(schedule, std::memory_or
 
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *block_tables, int32_t max_blocks,
-                                      const int32_t *prefix_lens, const int32_t *cu_suffix,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
-                                      int32_t B, int32_t num_q_heads, int32_t T,
-                                      int32_t max_row_tiles, float sm_scale, void *out,
+                                      int32_t B, int32_t num_q_heads, int32_t T, float sm_scale, void *out,
                                       hipStream_t s, int auto_schedule, int n_cu)
 {
-    (void)prefix_lens;   // the lengths travel in the work map, from the host copies
-    (void)cu_suffix;
-    (void)max_row_tiles;
     // The sequences with new tokens, longest context first.
     std::vector<int32_t> seq;
     seq.reserve((size_t)std::max(B, 0));

@@ -41,12 +41,12 @@ hipError_t launch_push_blocks(const void *pool_k, const void *pool_v, int32_t po
                               hipStream_t s);
 
 // Attention launcher (attn.hip).
+// The lengths travel in the launches' arguments (the work map), taken from the host
+// copies, which the caller guarantees equal the device arrays.
 hipError_t launch_prefix_prefill_attn(const void *q, const pcr_kv_pool &pool,
                                       const int32_t *block_tables, int32_t max_blocks,
-                                      const int32_t *prefix_lens, const int32_t *cu_suffix,
                                       const int32_t *host_prefix_lens, const int32_t *host_cu_suffix,
-                                      int32_t B, int32_t num_q_heads, int32_t T,
-                                      int32_t max_row_tiles, float sm_scale, void *out,
+                                      int32_t B, int32_t num_q_heads, int32_t T, float sm_scale, void *out,
                                       hipStream_t s, int auto_schedule, int n_cu);
 // Compute units of the current device (queried once per device).
 pcr_status device_cu_count(int32_t *n_cu, const char *who);
@@ -116,11 +116,10 @@ int attn_rows_per_workgroup(int head_dim);
 void attn_set_schedule(int schedule);
 
 // Every argument check of pcr_prefix_prefill_attn, with no launch (errors name `who`);
-// on success *T_out is the suffix token count (0: nothing to do) and *max_tiles_out
-// the largest row-tile count of a sequence.
+// on success *T_out is the suffix token count (0: nothing to do).
 pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
                       const int32_t *prefix_lens, const int32_t *cu_suffix, const int32_t *host_prefix_lens,
                       const int32_t *host_cu_suffix, int32_t B, int32_t num_q_heads, float sm_scale,
-                      const void *out, const char *who, int64_t *T_out, int64_t *max_tiles_out);
+                      const void *out, const char *who, int64_t *T_out);
 
 }  // namespace pcr

@@ -132,11 +132,11 @@ pcr_status run_pipeline(const pcr_layer_io *layers, const pcr_host_kv *offload_d
     // The attention's arguments, batch-wide and per layer, are checked before anything is
     // queued, so a bad scale, head count or length table leaves the streams untouched.
     for (int32_t l = 0; l < n_layers; ++l) {
-        int64_t T = 0, tiles = 0;
+        int64_t T = 0;
         pcr_status st = attn_check(layers[l].q, &layers[l].pool, batch->block_tables, batch->max_blocks,
                                    batch->prefix_lens, batch->cu_suffix, batch->host_prefix_lens,
                                    batch->host_cu_suffix, batch->B, batch->num_q_heads, batch->sm_scale,
-                                   layers[l].out, who, &T, &tiles);
+                                   layers[l].out, who, &T);
         if (st) return st;
     }
     hipStream_t cs = static_cast<hipStream_t>(copy_stream);

@@ -616,10 +616,9 @@ namespace pcr {
 pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *block_tables, int32_t max_blocks,
                       const int32_t *prefix_lens, const int32_t *cu_suffix, const int32_t *host_prefix_lens,
                       const int32_t *host_cu_suffix, int32_t B, int32_t num_q_heads, float sm_scale,
-                      const void *out, const char *who, int64_t *T_out, int64_t *max_tiles_out)
+                      const void *out, const char *who, int64_t *T_out)
 {
     *T_out = 0;
-    *max_tiles_out = 0;
     pcr_status st = check_pool(pool, who);
     if (st) return st;
     if (B < 0) return fail(PCR_ERR_INVALID_ARG, "%s: B < 0", who);
@@ -633,7 +632,7 @@ pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *blo
     if (host_cu_suffix[0] != 0) return fail(PCR_ERR_INVALID_ARG, "%s: cu_suffix[0] must be 0", who);
     const int G = num_q_heads / pool->num_kv_heads;
     const int rows_per_wg = attn_rows_per_workgroup(pool->head_dim);
-    int64_t max_tiles = 0;
+    int64_t tiles = 0;   // row tiles of all sequences at the finest schedule, one kv head
     for (int b = 0; b < B; ++b) {
         const int64_t s = (int64_t)host_cu_suffix[b + 1] - host_cu_suffix[b];
         if (s < 0 || host_prefix_lens[b] < 0)
@@ -641,7 +640,7 @@ pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *blo
         if (ceil_div((int64_t)host_prefix_lens[b] + s, kBlockSize) > max_blocks)
             return fail(PCR_ERR_INVALID_ARG, "%s: sequence %d needs more blocks than max_blocks %d", who, b,
                         max_blocks);
-        max_tiles = std::max<int64_t>(max_tiles, ceil_div(s * G, rows_per_wg));
+        tiles += ceil_div(s * G, rows_per_wg);
     }
     const int64_t T = host_cu_suffix[B];
     if (T == 0) return PCR_OK;
@@ -650,10 +649,11 @@ pcr_status attn_check(const void *q, const pcr_kv_pool *pool, const int32_t *blo
         return fail(PCR_ERR_INVALID_ARG, "%s: NULL device argument", who);
     if (((uintptr_t)q | (uintptr_t)out) & 15)
         return fail(PCR_ERR_INVALID_ARG, "%s: q/out must be 16-byte aligned", who);
-    if (max_tiles * pool->num_kv_heads * (int64_t)B > (int64_t)1 << 30)
-        return fail(PCR_ERR_UNSUPPORTED, "%s: batch too large for one launch", who);
+    // (each launch's grid, at most every tile of every kv head, stays far inside the
+    // 2^32 work items of one grid dimension)
+    if (tiles * pool->num_kv_heads > (int64_t)1 << 22)
+        return fail(PCR_ERR_UNSUPPORTED, "%s: batch too large", who);
     *T_out = T;
-    *max_tiles_out = max_tiles;
     return PCR_OK;
 }
 
@@ -861,17 +861,15 @@ pcr_status prefix_prefill_attn(const void *q, const pcr_kv_pool *pool, const int
                                int32_t num_q_heads, float sm_scale, void *out, void *stream, int auto_schedule)
 {
     g_err[0] = 0;
-    int64_t T = 0, max_tiles = 0;
+    int64_t T = 0;
     pcr_status st = attn_check(q, pool, block_tables, max_blocks, prefix_lens, cu_suffix, host_prefix_lens,
-                               host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T,
-                               &max_tiles);
+                               host_cu_suffix, B, num_q_heads, sm_scale, out, "pcr_prefix_prefill_attn", &T);
     if (st || T == 0) return st;
     int32_t n_cu = 0;
     st = device_cu_count(&n_cu, "pcr_prefix_prefill_attn");
     if (st) return st;
-    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, prefix_lens, cu_suffix,
-                                              host_prefix_lens, host_cu_suffix, B,
-                                              num_q_heads, (int32_t)T, (int32_t)max_tiles, sm_scale, out,
+    hipError_t e = launch_prefix_prefill_attn(q, *pool, block_tables, max_blocks, host_prefix_lens,
+                                              host_cu_suffix, B, num_q_heads, (int32_t)T, sm_scale, out,
                                               static_cast<hipStream_t>(stream), auto_schedule, n_cu);
     if (e != hipSuccess) return hip_fail(e, "pcr_prefix_prefill_attn: launch");
     return PCR_OK;
