@@ -217,7 +217,7 @@ __device__ __forceinline__ void decode_workgroup(const u16 *__restrict__ q, cons
     float m_run = -INFINITY, l_run = 0.f;
     if (kbeg < n_keys) {
         const u16 *qrow = q + (t0 * Hq + (col ? h : g * G)) * D + 8 * q4;
-        decode_wave::chunk<D, 2>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, bt_row, last_blk, kbeg, kend,
+        decode_wave::chunk<D, 2, true>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, bt_row, last_blk, kbeg, kend,
                                  scale_log2, o, m_run, l_run);
     } else {
 #pragma unroll

@@ -58,7 +58,7 @@ constexpr int waves_per_cu(int) { return 4; }
 constexpr int kMinChunk = 256;         // keys; shorter chunks spend more on set-up than on loads
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int D>
+template <int D, bool K_CACHED>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) void decode_split_kernel(
     const u16 *__restrict__ q, const u16 *__restrict__ pool_k, const u16 *__restrict__ pool_v,
     int32_t num_blocks, int32_t Hkv, const int32_t *__restrict__ block_tables, int32_t max_blocks,
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1))) v
     float m_run = -INFINITY, l_run = 0.f;
     if (active) {
         const u16 *qrow = q + ((int64_t)b * Hq + (col ? h : g * G)) * D + 8 * q4;
-        decode_wave::chunk<D, 3>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, block_tables + (int64_t)b * max_blocks,
+        decode_wave::chunk<D, 3, K_CACHED>(qrow, col, pool_k, pool_v, num_blocks, Hkv, g, block_tables + (int64_t)b * max_blocks,
                                  last_blk, kbeg, kend, scale_log2, o, m_run, l_run);
     } else {
 #pragma unroll
@@ -212,8 +212,9 @@ hipError_t decode_noalloc_scratch(void **ptr)
     return hipSuccess;
 }
 
-DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                       int32_t max_context, int32_t n_cu, const int32_t *ctx, int64_t ws_limit)
+namespace {
+DecodePlan decode_split_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                             int32_t max_context, int32_t n_cu, const int32_t *ctx, int64_t ws_limit)
 {
     DecodePlan p{};
     const int64_t pairs = (int64_t)B * num_kv_heads;
@@ -272,6 +273,21 @@ DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int
     p.workspace_bytes = ws;
     return p;
 }
+}  // namespace
+
+DecodePlan decode_plan(int32_t B, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t max_context, int32_t n_cu, const int32_t *ctx, int64_t ws_limit)
+{
+    DecodePlan p = decode_split_plan(B, num_q_heads, num_kv_heads, head_dim, max_context, n_cu, ctx, ws_limit);
+    // Non-temporal K loads when every sequence has one length and its chunks give every
+    // SIMD a wave: then every wave streams one chunk length for the whole kernel and HBM
+    // is the bound. Otherwise (ragged or small batches, bound by what each compute unit
+    // has in flight) ordinary K loads, which fetch each K line once per step.
+    bool same = ctx != nullptr;
+    for (int32_t b = 0; b < B && same; ++b) same = ctx[b] == max_context;
+    p.k_streamed = same && (int64_t)B * num_kv_heads * p.n_split >= (int64_t)n_cu * waves_per_cu(head_dim);
+    return p;
+}
 
 int decode_max_cols() { return kMaxCols; }
 
@@ -296,14 +312,16 @@ hipError_t launch_decode_attn(const void *q, const pcr_kv_pool &pool, const int3
     auto *pk = static_cast<const u16 *>(pool.k);
     auto *pv = static_cast<const u16 *>(pool.v);
     auto *oo = static_cast<u16 *>(out);
-    if (D == 128)
-        hipLaunchKernelGGL(decode_split_kernel<128>, grid, dim3(64 * wg_waves), lds, s, qq, pk, pv, pool.num_blocks,
-                           Hkv, block_tables, max_blocks, context_lens, B, num_q_heads, plan.n_split, plan.chunk,
-                           scale_log2, lds_merge, oo, ws_o, ws_ml);
-    else
-        hipLaunchKernelGGL(decode_split_kernel<64>, grid, dim3(64 * wg_waves), lds, s, qq, pk, pv, pool.num_blocks,
-                           Hkv, block_tables, max_blocks, context_lens, B, num_q_heads, plan.n_split, plan.chunk,
-                           scale_log2, lds_merge, oo, ws_o, ws_ml);
+    auto split = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, grid, dim3(64 * wg_waves), lds, s, qq, pk, pv, pool.num_blocks, Hkv, block_tables,
+                           max_blocks, context_lens, B, num_q_heads, plan.n_split, plan.chunk, scale_log2, lds_merge,
+                           oo, ws_o, ws_ml);
+    };
+    if (D == 128) {
+        if (plan.k_streamed) split(decode_split_kernel<128, false>); else split(decode_split_kernel<128, true>);
+    } else {
+        if (plan.k_streamed) split(decode_split_kernel<64, false>); else split(decode_split_kernel<64, true>);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !through_ws) return e;
     const dim3 cgrid((unsigned)(((int64_t)B * num_q_heads + kWaves - 1) / kWaves));

@@ -64,6 +64,7 @@ struct DecodePlan {
     int32_t chunk;
     int32_t lds_merge;
     int32_t ws_wg_waves;   // waves per workgroup when chunks merge through the workspace
+    int32_t k_streamed;    // every sequence of one length: K loads non-temporal
     int64_t workspace_bytes;
     int64_t bound_workspace_bytes;
 };
