@@ -14,9 +14,11 @@
 // one wave (decode_wave::chunk, decode_wave.h: the G query heads as MFMA columns,
 // K and V straight from HBM into registers, here with three register sets so that
 // two steps of loads are in flight while a third is used); the host picks n_split
-// so that every SIMD gets about one wave. The loads are non-temporal: every byte
-// is used once, and streaming them past the caches measured about 10% faster than
-// ordinary loads.
+// so that every SIMD gets about one wave. Every byte is used once: V loads are
+// non-temporal, and K loads too when every sequence has one length and the chunks
+// give every SIMD a wave (the kernel then streams HBM at full rate, where bypassing
+// the caches measured about 10% faster than ordinary loads for both); otherwise K
+// loads are ordinary ones (decode_wave.h: K_CACHED).
 //
 // A chunk that covers its whole sequence writes the output row. Up to four
 // chunks of one (sequence, kv head) form one workgroup and are merged through
