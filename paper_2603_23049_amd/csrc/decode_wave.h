@@ -16,9 +16,9 @@
 // a column. NSETS register sets of one step's K/V rotate (NSETS - 1 steps in flight
 // while one is used). Every byte is used once, so V loads are non-temporal; K loads are
 // non-temporal too when the caller streams HBM at full rate with every wave (K_CACHED
-// false), and ordinary loads otherwise: the two products of a step read the two
-// 64-byte halves of each 128-byte K line, which an ordinary load lets the vector L1
-// fetch once. Measured: a compute unit running one decode workgroup alone moved 37 GB/s
+// false), and ordinary loads otherwise: a key row's 128-byte lines are read in two
+// 64-byte halves by two load instructions (dims 32*kk .. for kk = 0, 1 and 2, 3), and
+// an ordinary load lets the vector L1 fetch each line once. Measured: a compute unit running one decode workgroup alone moved 37 GB/s
 // with non-temporal K loads and 47 GB/s with ordinary ones, while a batch that keeps
 // HBM busy with every wave ran 2% slower with ordinary K loads.
 //
