@@ -165,19 +165,48 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(
     const int ns = min((n_keys + chunk - 1) / chunk, n_split);
     if (ns <= 1) return;                            // written by the split kernel
     const int64_t part0 = ((int64_t)b * Hkv + g) * n_split * G + c;
-    float M = -INFINITY;
-    for (int k = 0; k < ns; ++k) M = fmaxf(M, ws_ml[2 * (part0 + (int64_t)k * G)]);
-    float L = 0.f, acc[E];
+    // Up to 64 chunks per pass: lane j reads chunk k0 + j's max and sum (all loads in
+    // flight together), the wave reduces them, and the O rows are read eight chunks at a
+    // time with their loads issued before any is used. Across passes the running max,
+    // sum and accumulator are rescaled. The accumulator adds the chunks in their order.
+    float M = -INFINITY, L = 0.f, acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
-    for (int k = 0; k < ns; ++k) {
-        const int64_t part = part0 + (int64_t)k * G;
-        const f32x2 ml = *reinterpret_cast<const f32x2 *>(ws_ml + 2 * part);
-        const float w = __builtin_amdgcn_exp2f(ml[0] - M);
-        L += w * ml[1];
-        const float *po = ws_o + part * D + E * lane;
+    for (int k0 = 0; k0 < ns; k0 += 64) {
+        const int nk = min(64, ns - k0);
+        f32x2 ml = f32x2{-INFINITY, 0.f};
+        if (lane < nk) ml = *reinterpret_cast<const f32x2 *>(ws_ml + 2 * (part0 + (int64_t)(k0 + lane) * G));
+        float mb = ml[0];
 #pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] += w * po[e];
+        for (int off = 32; off >= 1; off >>= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+        const float Mn = fmaxf(M, mb);                  // finite: chunk k0 has keys
+        const float r = __builtin_amdgcn_exp2f(M - Mn);  // 0 on the first pass
+        M = Mn;
+        const float w = __builtin_amdgcn_exp2f(ml[0] - M);   // 0 past the last chunk
+        float lw = w * ml[1];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) lw += __shfl_xor(lw, off);
+        L = L * r + lw;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] *= r;
+        for (int j0 = 0; j0 < nk; j0 += 8) {
+            float po[8][E];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int j = min(j0 + i, nk - 1);       // a chunk past nk is reread, weight 0
+                const float *src = ws_o + (part0 + (int64_t)(k0 + j) * G) * D + E * lane;
+#pragma unroll
+                for (int e = 0; e < E; ++e) po[i][e] = src[e];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const float wi = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), min(j0 + i, 63)));
+                const float wv = j0 + i < nk ? wi : 0.f;
+#pragma unroll
+                for (int e = 0; e < E; ++e) acc[e] += wv * po[i][e];
+            }
+        }
     }
     const float inv = 1.f / L;
     u16 *orow = out + ((int64_t)b * Hq + h) * D + E * lane;
