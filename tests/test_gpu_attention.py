@@ -90,6 +90,28 @@ def test_edge_shapes(d, G):
     _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"edges d={d} G={G}")
 
 
+@pytest.mark.parametrize("G,Hkv,d", [(24, 2, 128), (32, 2, 64), (64, 1, 128)])
+def test_wide_groups(G, Hkv, d):
+    """More than 16 query heads per kv head: one-token rows then take prefill tiles
+    (the decode workgroups hold at most 16 heads), and a token's heads span several
+    32-row wave slices and 128-row tiles."""
+    pl, sl = [], []
+    for p in [0, 17, 256]:
+        for s in [1, 2, 63]:
+            pl.append(p)
+            sl.append(s)
+    pl.append(100)
+    sl.append(300)
+    nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl)) + 5
+    b = synth.ragged_batch("wide", Hq=Hkv * G, Hkv=Hkv, d=d, prefix_lens=pl, suffix_lens=sl,
+                           pool_blocks=nblocks, seed=70 + G)
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say(f"[gpu] attention wide groups G={G} Hkv={Hkv} d={d} B={b.B} T={b.T}")
+    L = _run(b, data, pk0, pv0)
+    _check(L.out_f64(), _oracle(b, data, pk0, pv0), f"wide G={G} d={d}")
+
+
 @pytest.mark.parametrize("B", [100, 140])
 def test_many_sequences(B):
     """More sequences than one lane of the work-map lookup holds (slots 64.. are read by
