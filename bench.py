@@ -1072,8 +1072,8 @@ def main(argv=None):
         args.no_pipeline = args.no_cpu_baseline = args.no_load = args.no_extra = args.no_clocks = True
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this path has no cross-GPU exchange and every box here "
-              "has one GPU; run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only (the path exchanges nothing between GPUs: each GPU "
+              "would run its own share of the batch); run with --gpus 1", file=sys.stderr)
         return 2
 
     # The oracle's library must be current before the GPU is initialised: building it
