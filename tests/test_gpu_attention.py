@@ -5,6 +5,8 @@ mean |err| <= 2e-3 against the fp64 oracle. Beyond the tolerance the HIP path
 must be deterministic and bit-invariant to which physical blocks hold the KV.
 Each test runs under both workgroup schedules (key halves, row halves).
 """
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -242,6 +244,42 @@ def test_rag_mix_sampled_rows_and_pool():
                            b.num_kv_heads, BS, rows=rows)
     got = L.out_f64()[rows[:, 0], rows[:, 1]]
     _check(got, want, "rag_mix sampled")
+
+
+@functools.lru_cache(maxsize=1)
+def _mixed_full_case():
+    """RAG-mix request lengths + 64 decode rows of 4352 keys, with one layer's data
+    (drawn once for both schedules)."""
+    from paper_2603_23049_amd import prefix_tree
+    rag = prefix_tree.rag_mix_batch()
+    n_dec, ctx = 64, 4352
+    pl = list(rag.prefix_lens) + [ctx - 1] * n_dec
+    sl = list(rag.suffix_lens) + [1] * n_dec
+    nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl))
+    b = synth.ragged_batch("mixed_full", Hq=rag.num_q_heads, Hkv=rag.num_kv_heads, d=rag.head_dim,
+                           prefix_lens=pl, suffix_lens=sl, pool_blocks=nblocks, seed=4352)
+    return b, synth.make_layer(b), sl, n_dec, ctx
+
+
+def test_mixed_rag_and_decode_rows_full_size():
+    """The benchmark's mixed launch: the RAG mix's 16 request lengths plus 64 decode rows
+    of 4352 keys (32 q / 8 kv heads, d = 128) in one launch, decode rows spread over the
+    prefill tiles. Every head of every decode row, and the first, middle and last rows of
+    every request, against the oracle."""
+    b, data, sl, n_dec, ctx = _mixed_full_case()
+    shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
+    zero = np.zeros(shape, np.uint16)
+    say(f"[gpu] attention mixed full size: rag mix + {n_dec} decode rows of {ctx} keys (T={b.T})")
+    L = _run(b, data, zero, zero)
+    cu = b.cu_suffix
+    toks = []
+    for i, s in enumerate(sl):
+        toks += sorted({int(cu[i]) + t for t in (0, s // 2, s - 1)})
+    heads = range(b.num_q_heads)
+    rows = np.array([[t, h] for t in toks for h in heads], np.int32)
+    want = _oracle(b, data, zero, zero, rows=rows)
+    got = L.out_f64()[rows[:, 0], rows[:, 1]]
+    _check(got, want, "mixed full size")
 
 
 def test_long_context_128k_sampled_rows():
