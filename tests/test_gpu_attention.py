@@ -246,27 +246,29 @@ def test_rag_mix_sampled_rows_and_pool():
     _check(got, want, "rag_mix sampled")
 
 
-@functools.lru_cache(maxsize=1)
-def _mixed_full_case():
-    """RAG-mix request lengths + 64 decode rows of 4352 keys, with one layer's data
+@functools.lru_cache(maxsize=2)
+def _mixed_full_case(n_dec):
+    """RAG-mix request lengths + n_dec decode rows of 4352 keys, with one layer's data
     (drawn once for both schedules)."""
     from paper_2603_23049_amd import prefix_tree
     rag = prefix_tree.rag_mix_batch()
-    n_dec, ctx = 64, 4352
+    ctx = 4352
     pl = list(rag.prefix_lens) + [ctx - 1] * n_dec
     sl = list(rag.suffix_lens) + [1] * n_dec
     nblocks = sum(-(-(p + s) // BS) for p, s in zip(pl, sl))
     b = synth.ragged_batch("mixed_full", Hq=rag.num_q_heads, Hkv=rag.num_kv_heads, d=rag.head_dim,
-                           prefix_lens=pl, suffix_lens=sl, pool_blocks=nblocks, seed=4352)
-    return b, synth.make_layer(b), sl, n_dec, ctx
+                           prefix_lens=pl, suffix_lens=sl, pool_blocks=nblocks, seed=4352 + n_dec)
+    return b, synth.make_layer(b), sl, ctx
 
 
-def test_mixed_rag_and_decode_rows_full_size():
-    """The benchmark's mixed launch: the RAG mix's 16 request lengths plus 64 decode rows
+@pytest.mark.parametrize("n_dec", [64, 256])
+def test_mixed_rag_and_decode_rows_full_size(n_dec):
+    """The benchmark's mixed launches: the RAG mix's 16 request lengths plus 64 decode rows
     of 4352 keys (32 q / 8 kv heads, d = 128) in one launch, decode rows spread over the
-    prefill tiles. Every head of every decode row, and the first, middle and last rows of
-    every request, against the oracle."""
-    b, data, sl, n_dec, ctx = _mixed_full_case()
+    prefill tiles; with 256 decode rows, three launches of the sequences dealt round robin.
+    Every head of every decode row, and the first, middle and last rows of every request,
+    against the oracle."""
+    b, data, sl, ctx = _mixed_full_case(n_dec)
     shape = (b.pool_blocks, b.num_kv_heads, BS * b.head_dim)
     zero = np.zeros(shape, np.uint16)
     say(f"[gpu] attention mixed full size: rag mix + {n_dec} decode rows of {ctx} keys (T={b.T})")
