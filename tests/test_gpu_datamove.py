@@ -113,6 +113,40 @@ def test_gather_bitexact(d):
     assert np.array_equal(u16(k_out), wk) and np.array_equal(u16(v_out), wv)
 
 
+@pytest.mark.parametrize("layout", ["block_order", "ragged_300"])
+def test_append_sweep_size_bitexact(layout):
+    """The append sweep's largest size: 131072 new tokens (8 kv heads, d = 128: 512 MiB
+    of K+V read and written), either in block order over a random order of the pool's
+    blocks, or as sequences of 300 tokens each starting at a block of its own, so that
+    the kernel's tiles start inside the sequences' 8-slot V chunks. The whole pool
+    (canaries in every slot the list does not name) equals the oracle's bit for bit."""
+    T, Hkv, d = 131072, 8, 128
+    rng = np.random.Generator(np.random.PCG64(131 + len(layout)))
+    t = np.arange(T, dtype=np.int64)
+    if layout == "block_order":
+        nb = -(-T // BS)
+        blocks = rng.permutation(nb).astype(np.int64)
+        slots = blocks[t // BS] * BS + t % BS
+    else:
+        seq, per_seq = 300, -(-300 // BS)
+        nb = -(-T // seq) * per_seq
+        blocks = rng.permutation(nb).astype(np.int64)
+        pos = t % seq
+        slots = blocks[(t // seq) * per_seq + pos // BS] * BS + pos % BS
+    slots = slots.astype(np.int32)
+    shape = (nb, Hkv, BS * d)
+    pk0, pv0 = synth.normal_bf16(rng, shape), synth.normal_bf16(rng, shape)
+    k_new, v_new = synth.normal_bf16(rng, (T, Hkv, d)), synth.normal_bf16(rng, (T, Hkv, d))
+    say(f"[gpu] append sweep size {layout}: T={T} blocks={nb}")
+    pool = pcr.KVPool(dev(pk0), dev(pv0), Hkv, d)
+    pcr.append_kv(pool, dev(k_new), dev(v_new), dev(slots))
+    torch.cuda.synchronize()
+    want_k, want_v = pk0.copy(), pv0.copy()
+    odm.append(want_k, want_v, k_new, v_new, slots, BS)
+    assert np.array_equal(u16(pool.k), want_k), "K pool differs after append"
+    assert np.array_equal(u16(pool.v), want_v), "V pool differs after append"
+
+
 def test_append_empty_and_load_empty_are_noops():
     b = synth.tiny()
     data = synth.make_layer(b)
