@@ -218,6 +218,24 @@ def test_l70b_shape_sampled_rows():
     _check(got, want, "l70b sampled")
 
 
+def test_l70b_tp8_shard_sampled_rows():
+    """One GPU's share of the 70B-shaped layer at tensor parallelism 8 (8 q heads, 1 kv
+    head, p = 15360, s = 1024): a kv-head count that is not a multiple of the XCD count
+    (the work map's padded order). Every head of a spread of tokens, including the first
+    and last suffix row of both sequences."""
+    b = synth.uniform_batch("l70b_tp8_shard", B=2, Hq=8, Hkv=1, d=128, p=15360, s=1024, pool_blocks=4096,
+                            seed=5)
+    data = synth.make_layer(b)
+    pk0, pv0 = _pools(b)
+    say("[gpu] attention l70b tp8 shard (sampled rows)")
+    L = _run(b, data, pk0, pv0)
+    toks = sorted(set([0, 1, 511, 1023, 1024, 1025, 2047] + list(range(53, 2048, 173))))
+    rows = np.array([[t, h] for t in toks for h in range(b.num_q_heads)], np.int32)
+    want = _oracle(b, data, pk0, pv0, rows=rows)
+    got = L.out_f64()[rows[:, 0], rows[:, 1]]
+    _check(got, want, "tp8 shard sampled")
+
+
 def test_rag_mix_sampled_rows_and_pool():
     """RAG-mix batch (16 ragged requests, prefixes hit in a warmed prefix tree, shared
     tree chunks loaded once, two sequences with no hit): the pool after load + append is
